@@ -1,0 +1,259 @@
+// C ABI of libflowblock.so: argument validation, workspace sizing and launch.
+// Every entry point validates what the host can see before enqueueing
+// anything, returns an FB_* status and keeps a thread-local message for
+// fb_last_error().  No exception crosses the ABI.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "internal.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_err[0] = 0;
+    return FB_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(FB_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// Compute units of the current device, cached per device ordinal.
+int cu_count() {
+    static thread_local int cached_dev = -1;
+    static thread_local int cached_cus = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev != cached_dev) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                hipSuccess || cus <= 0)
+            cus = 256;
+        cached_dev = dev;
+        cached_cus = cus;
+    }
+    return cached_cus;
+}
+
+int check_pack(const fb_pack* p) {
+    if (!p) return fail(FB_E_INVAL, "pack is NULL");
+    if (!p->buf) return fail(FB_E_INVAL, "pack buffer is NULL (call fb_pack_init)");
+    if (p->B < 1 || p->W_max < 1 || p->bl < 1)
+        return fail(FB_E_INVAL, "pack capacities are not initialised");
+    if (p->row_cap != p->B * p->W_max * p->bl || p->tile_cap != p->B * p->W_max)
+        return fail(FB_E_INVAL, "pack capacities are inconsistent");
+    return FB_OK;
+}
+
+int check_shape(const fb_pack* p, const fb_attn_shape* sh) {
+    if (!sh) return fail(FB_E_INVAL, "shape is NULL");
+    if (sh->Hq < 1 || sh->Hkv < 1 || sh->Hq % sh->Hkv)
+        return fail(FB_E_INVAL, "need Hq >= 1, Hkv >= 1 and Hq %% Hkv == 0 (got %d, %d)",
+                    sh->Hq, sh->Hkv);
+    if (sh->head_dim != 32 && sh->head_dim != 64 && sh->head_dim != 128)
+        return fail(FB_E_UNSUPPORTED, "head_dim %d not built (32, 64, 128)", sh->head_dim);
+    if (sh->dtype != FB_BF16 && sh->dtype != FB_F32)
+        return fail(FB_E_UNSUPPORTED, "dtype %d not supported", sh->dtype);
+    if (!is_pow2(sh->page_size))
+        return fail(FB_E_INVAL, "page_size %d is not a power of two", sh->page_size);
+    if (sh->dtype == FB_BF16 && sh->page_size < 8)
+        return fail(FB_E_UNSUPPORTED, "bf16 needs page_size >= 8 (got %d)", sh->page_size);
+    if (sh->max_pages < 1 || sh->num_pages < 1)
+        return fail(FB_E_INVAL, "max_pages and num_pages must be >= 1");
+    if (sh->kv_split < 0 || sh->kv_split % 32)
+        return fail(FB_E_INVAL, "kv_split %d must be 0 or a positive multiple of 32",
+                    sh->kv_split);
+    const size_t elt = sh->dtype == FB_BF16 ? 2 : 4;
+    if ((size_t)p->bl * sh->head_dim * elt > 65536)
+        return fail(FB_E_UNSUPPORTED, "bl*head_dim too large for the KV staging buffer");
+    if (isnan(sh->sm_scale) || isinf(sh->sm_scale))
+        return fail(FB_E_INVAL, "sm_scale is not finite");
+    return FB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fb_version(void) { return "flowblock 0.1.0 gfx950"; }
+
+const char* fb_last_error(void) { return g_err; }
+
+size_t fb_pack_bytes(int B, int W_max, int bl) {
+    if (B < 1 || W_max < 1 || bl < 1) return 0;
+    size_t o[8];
+    fb::pack_offsets_ints(B, B * W_max, B * W_max * bl, o);
+    return o[7] * sizeof(int32_t);
+}
+
+int fb_pack_get_offsets(int B, int W_max, int bl, fb_pack_offsets* off) {
+    if (!off) return fail(FB_E_INVAL, "offsets is NULL");
+    if (B < 1 || W_max < 1 || bl < 1) return fail(FB_E_INVAL, "B, W_max, bl must be >= 1");
+    size_t o[8];
+    fb::pack_offsets_ints(B, B * W_max, B * W_max * bl, o);
+    off->header = o[0] * 4;
+    off->tiles = o[1] * 4;
+    off->req_w = o[2] * 4;
+    off->req_row0 = o[3] * 4;
+    off->row_req = o[4] * 4;
+    off->row_pos = o[5] * 4;
+    off->row_tok = o[6] * 4;
+    off->total = o[7] * 4;
+    return ok();
+}
+
+int fb_pack_init(fb_pack* pack, void* buf, size_t buf_bytes, int B, int W_max, int bl,
+                 int layout) {
+    if (!pack) return fail(FB_E_INVAL, "pack is NULL");
+    if (!buf) return fail(FB_E_INVAL, "buf is NULL");
+    if (B < 1 || W_max < 1 || bl < 1)
+        return fail(FB_E_INVAL, "B, W_max, bl must be >= 1 (got %d, %d, %d)", B, W_max, bl);
+    if ((long long)B * W_max * bl > (1LL << 30))
+        return fail(FB_E_INVAL, "B*W_max*bl exceeds 2^30 rows");
+    if (W_max > 64) return fail(FB_E_UNSUPPORTED, "W_max %d > 64", W_max);
+    if (layout != FB_RAGGED && layout != FB_PADDED)
+        return fail(FB_E_INVAL, "layout %d is neither FB_RAGGED nor FB_PADDED", layout);
+    if (!aligned16(buf)) return fail(FB_E_INVAL, "pack buffer must be 16-byte aligned");
+    const size_t need = fb_pack_bytes(B, W_max, bl);
+    if (buf_bytes < need)
+        return fail(FB_E_WORKSPACE, "pack buffer has %zu bytes, needs %zu", buf_bytes, need);
+    pack->buf = buf;
+    pack->B = B;
+    pack->W_max = W_max;
+    pack->bl = bl;
+    pack->layout = layout;
+    pack->row_cap = B * W_max * bl;
+    pack->tile_cap = B * W_max;
+    return ok();
+}
+
+int fb_pack_wavefronts(const fb_req_state* st, const int32_t* tokens, int n_max, int T_max,
+                       fb_pack* pack, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    if (!st) return fail(FB_E_INVAL, "state is NULL");
+    if (n_max < 1 || T_max < 1) return fail(FB_E_INVAL, "n_max and T_max must be >= 1");
+    hipError_t e = fb::launch_pack(st, tokens, n_max, T_max, pack, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "pack launch");
+    return ok();
+}
+
+int fb_pack_read_status(const fb_pack* pack, int* code, int* request, int* n_rows,
+                        int* n_tiles, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    int32_t hdr[fb::kHdrInts];
+    hipError_t e = hipMemcpyAsync(hdr, pack->buf, sizeof hdr, hipMemcpyDeviceToHost,
+                                  (hipStream_t)stream);
+    if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "reading the pack status");
+    const int32_t key = hdr[fb::kHdrStatus];
+    if (code) *code = key == FB_PACK_STATUS_NONE ? FB_DERR_NONE : (key & 15);
+    if (request) *request = key == FB_PACK_STATUS_NONE ? -1 : (key >> 4);
+    if (n_rows) *n_rows = hdr[fb::kHdrRows];
+    if (n_tiles) *n_tiles = hdr[fb::kHdrTiles];
+    return ok();
+}
+
+int fb_write_window_kv(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                       const int32_t* page_table, const fb_pack* pack,
+                       const fb_attn_shape* sh, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_shape(pack, sh);
+    if (rc) return rc;
+    if (!k_new || !v_new || !k_cache || !v_cache || !page_table)
+        return fail(FB_E_INVAL, "a tensor pointer is NULL");
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) || !aligned16(v_cache))
+        return fail(FB_E_INVAL, "K/V pointers must be 16-byte aligned");
+    hipError_t e = fb::launch_write_kv(k_new, v_new, k_cache, v_cache, page_table, pack, sh,
+                                       (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "KV write launch");
+    return ok();
+}
+
+size_t fb_attention_workspace_bytes(const fb_pack* pack, const fb_attn_shape* sh) {
+    if (check_pack(pack) || check_shape(pack, sh)) return 0;
+    return fb::attention_sizes(pack, sh, cu_count()).total;
+}
+
+int fb_wavefront_attention(const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* page_table, const fb_pack* pack,
+                           const fb_attn_shape* sh, void* out, void* ws, size_t ws_bytes,
+                           void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_shape(pack, sh);
+    if (rc) return rc;
+    if (!q || !k_cache || !v_cache || !page_table || !out)
+        return fail(FB_E_INVAL, "a tensor pointer is NULL");
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
+        return fail(FB_E_INVAL, "q, caches and out must be 16-byte aligned");
+    const fb::AttnPlanSizes z = fb::attention_sizes(pack, sh, cu_count());
+    if (ws_bytes < z.total || (z.total > 0 && !ws))
+        return fail(FB_E_WORKSPACE, "attention workspace has %zu bytes, needs %zu", ws_bytes,
+                    z.total);
+    if (ws && !aligned16(ws)) return fail(FB_E_INVAL, "workspace must be 16-byte aligned");
+    hipError_t e = fb::launch_attention(q, k_cache, v_cache, page_table, pack, sh, out, ws, z,
+                                        (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "attention launch");
+    return ok();
+}
+
+size_t fb_update_workspace_bytes(const fb_pack* pack, int V) {
+    if (check_pack(pack) || V < 1) return 0;
+    return fb::update_sizes(pack, V, cu_count()).total;
+}
+
+int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int T_max,
+                      float* conf, int32_t* argmax, fb_req_state* st, uint8_t* pe,
+                      uint8_t* fin, int n_max, const fb_pack* pack,
+                      const fb_update_params* prm, fb_req_stats* stats, void* ws,
+                      size_t ws_bytes, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    if (!logits || !tokens || !conf || !argmax || !st || !pe || !fin || !prm)
+        return fail(FB_E_INVAL, "a required pointer is NULL");
+    if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
+    if (dtype != FB_BF16 && dtype != FB_F32)
+        return fail(FB_E_UNSUPPORTED, "logit dtype %d not supported", dtype);
+    if (!aligned16(logits)) return fail(FB_E_INVAL, "logits must be 16-byte aligned");
+    if (T_max < 1 || n_max < 1) return fail(FB_E_INVAL, "T_max and n_max must be >= 1");
+    if (prm->W < 1 || prm->W > pack->W_max)
+        return fail(FB_E_INVAL, "W %d outside [1, W_max=%d]", prm->W, pack->W_max);
+    if (prm->S_pe < 0) return fail(FB_E_INVAL, "S_pe must be >= 0");
+    if (prm->mask_id < 0 || prm->mask_id >= V)
+        return fail(FB_E_INVAL, "mask_id %d outside [0, V)", prm->mask_id);
+    if (isnan(prm->tau_mask) || isnan(prm->tau_edit) || isnan(prm->theta_spawn))
+        return fail(FB_E_INVAL, "a threshold is NaN");
+    if (prm->flags & ~(FB_EDIT_MASKED | FB_FORCE_PROGRESS))
+        return fail(FB_E_INVAL, "unknown flag bits 0x%x", prm->flags);
+    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
+    if (ws_bytes < z.total || !ws)
+        return fail(FB_E_WORKSPACE, "update workspace has %zu bytes, needs %zu", ws_bytes,
+                    z.total);
+    if (!aligned16(ws)) return fail(FB_E_INVAL, "workspace must be 16-byte aligned");
+    hipError_t e = fb::launch_update(logits, V, dtype, tokens, T_max, conf, argmax, st, pe,
+                                     fin, n_max, pack, prm, stats, ws, z,
+                                     (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "update launch");
+    return ok();
+}
+
+}  // extern "C"

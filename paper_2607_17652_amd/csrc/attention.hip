@@ -1,0 +1,643 @@
+// W-shaped block-causal window attention (Sec. 4.1; Eq. 5 per packed row).
+//
+// The mask of Eq. 5 reduces, for window slot s of request b, to one key count
+// kv_len = o_b + (s+1)*bl: every query of that block sees keys [0, kv_len) of
+// its KV head -- the frozen prefix, the earlier live blocks and its own block.
+// So the work is a set of independent "prefix attentions", one per
+// (live block, KV head), each with bl*(Hq/Hkv) query rows sharing one K/V
+// stream (GQA rows packed together).
+//
+// Work decomposition (all shapes fixed by capacity, so graph-capturable):
+//   unit  = (tile, KV head, 128-row group); rows are the block's
+//           (position, head-in-group) pairs flattened position-major
+//   item  = a unit's key range [kb, ke), a multiple of 32 keys long except at
+//           kv_len; long units are split so the grid has enough items
+//   plan_kernel    one workgroup: counts key tiles, picks the split size,
+//                  emits items, per-unit split counts and partial slots
+//   attn_bf16      one workgroup (4 waves x 32 rows) per item: 32-key K and
+//                  V^T tiles double-buffered in LDS, S^T = K Q^T and
+//                  O^T += V^T P^T on v_mfma_f32_32x32x16_bf16, online softmax
+//                  in the exp2 domain with lazy rescaling
+//   combine        merges split partials with their log-sum-exp weights
+//   attn_f32       a plain fp32 path (small problems, exactness reference)
+#include "internal.h"
+
+namespace fb {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kRowsPerWg = 128;     // 4 waves x 32 query rows
+constexpr int kAttnThreads = 256;
+constexpr int kKeyTile = 32;
+constexpr int kMinChunkTiles = 4;   // never split below 128 keys
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRescaleSlack = 8.0f;  // lazy rescale: running max may lag by 2^8
+
+enum ItemField { kIUnit = 0, kIKb, kIKe, kISlot };
+enum UnitField { kUSplits = 0, kUSlot0 };
+enum CountField { kCItems = 0, kCUnits, kCChunk };
+
+struct AttnWs {
+    int32_t* items;    // [item_cap][4]
+    int32_t* units;    // [unit_cap][2]
+    int32_t* counts;   // [4]
+    float* part_o;     // [slot_cap][128][D]
+    float* part_lse;   // [slot_cap][128]
+};
+
+// ---------------------------------------------------------------- plan ----
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanWaves = kPlanThreads / 64;
+
+__device__ long long wg_sum_ll(long long v, long long* lds) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) lds[wave] = v;
+    __syncthreads();
+    long long s = 0;
+    for (int w = 0; w < kPlanWaves; ++w) s += lds[w];
+    __syncthreads();
+    return s;
+}
+
+__device__ int wg_excl_scan(int v, int* lds, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) lds[wave] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int w = 0; w < kPlanWaves; ++w) {
+            int t = lds[w];
+            lds[w] = acc;
+            acc += t;
+        }
+        lds[kPlanWaves] = acc;
+    }
+    __syncthreads();
+    const int excl = lds[wave] + x - v;
+    *total = lds[kPlanWaves];
+    __syncthreads();
+    return excl;
+}
+
+// Key tiles of unit u; 0 (skip) when its keys run past the page table.
+__device__ inline int unit_key_tiles(const int32_t* tiles, int u, int per_tile,
+                                     long long max_keys) {
+    const int t = u / per_tile;
+    const int kv = tiles[(size_t)t * kTileInts + kTKvLen];
+    if ((long long)kv > max_keys) return 0;
+    return (kv + kKeyTile - 1) / kKeyTile;
+}
+
+__global__ void __launch_bounds__(kPlanThreads)
+plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
+            int target_items, int fixed_chunk_tiles, long long max_keys) {
+    __shared__ long long sum_lds[kPlanWaves];
+    __shared__ int scan_lds[kPlanWaves + 1];
+    const int n_tiles = pv.hdr[kHdrTiles];
+    const int per_tile = Hkv * RG;
+    const int n_units = n_tiles * per_tile;
+
+    long long my_tiles = 0;
+    for (int u = threadIdx.x; u < n_units; u += kPlanThreads)
+        my_tiles += unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+    const long long total_tiles = wg_sum_ll(my_tiles, sum_lds);
+
+    long long chunk = fixed_chunk_tiles;
+    if (chunk <= 0) {
+        chunk = (total_tiles + target_items - 1) / target_items;
+        if (chunk < kMinChunkTiles) chunk = kMinChunkTiles;
+    }
+    // Grow the split size until the items and partial slots fit.
+    for (;;) {
+        long long my_items = 0, my_slots = 0;
+        for (int u = threadIdx.x; u < n_units; u += kPlanThreads) {
+            const long long kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+            const long long ns = (kt + chunk - 1) / chunk;
+            my_items += ns;
+            if (ns > 1) my_slots += ns;
+        }
+        const long long items = wg_sum_ll(my_items, sum_lds);
+        const long long slots = wg_sum_ll(my_slots, sum_lds);
+        if (items <= item_cap && slots <= slot_cap) break;
+        chunk *= 2;
+    }
+
+    int items_before = 0, slots_before = 0;
+    for (int base = 0; base < n_units; base += kPlanThreads) {
+        const int u = base + threadIdx.x;
+        int ns = 0, kt = 0;
+        if (u < n_units) {
+            kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+            ns = (int)((kt + chunk - 1) / chunk);
+            if (kt == 0)
+                record_error(pv.hdr, pv.tiles[(size_t)(u / per_tile) * kTileInts + kTB],
+                             FB_DERR_PAGE);
+        }
+        int tot_items, tot_slots;
+        const int item0 = items_before + wg_excl_scan(ns, scan_lds, &tot_items);
+        const int slot0 = slots_before + wg_excl_scan(ns > 1 ? ns : 0, scan_lds, &tot_slots);
+        if (u < n_units) {
+            const int t = u / per_tile;
+            const int kv = pv.tiles[(size_t)t * kTileInts + kTKvLen];
+            ws.units[(size_t)u * 2 + kUSplits] = ns;
+            ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot0 : -1;
+            for (int k = 0; k < ns; ++k) {
+                int32_t* it = ws.items + (size_t)(item0 + k) * 4;
+                const long long kb = (long long)k * chunk * kKeyTile;
+                long long ke = kb + chunk * kKeyTile;
+                if (ke > kv) ke = kv;
+                it[kIUnit] = u;
+                it[kIKb] = (int)kb;
+                it[kIKe] = (int)ke;
+                it[kISlot] = ns > 1 ? slot0 + k : -1;
+            }
+        }
+        items_before += tot_items;
+        slots_before += tot_slots;
+    }
+    if (threadIdx.x == 0) {
+        ws.counts[kCItems] = items_before;
+        ws.counts[kCUnits] = n_units;
+        ws.counts[kCChunk] = (int)(chunk * kKeyTile);
+    }
+}
+
+// --------------------------------------------------------- bf16 MFMA ------
+// S^T accumulator layout of v_mfma_f32_32x32x16_bf16 (32x32 fp32 result):
+// lane l holds column l%32 and rows (i/4)*8 + (l/32)*4 + i%4 for i = 0..15.
+// Loading K row perm(m) into A-row m, with perm swapping index bits 2 and 3,
+// makes lane l's value i belong to tile key 16*(i/8) + 8*(l/32) + i%8, i.e.
+// eight consecutive keys per MFMA k-step -- exactly the k-slots the PV
+// product needs from P^T, so P moves from the S^T accumulator into the B
+// operand of the PV MFMA without any data exchange.
+__device__ inline int swap_bits23(int m) {
+    return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+__device__ inline float wave_xor32_max(float x) {
+    return fmaxf(x, __shfl_xor(x, 32, 64));
+}
+
+template <int D>
+struct __attribute__((aligned(16))) Bf16Tiles {
+    static constexpr int kRowK = D + 8;            // K tile row, padded
+    static constexpr int kRowV = kKeyTile + 8;     // V^T tile row, padded
+    uint16_t k[2][kKeyTile * kRowK];
+    uint16_t v[2][D * kRowV];
+};
+
+template <int D>
+__global__ void __launch_bounds__(kAttnThreads)
+attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
+                 const uint16_t* __restrict__ v_cache,
+                 const int32_t* __restrict__ page_table, PackView pv, AttnWs ws,
+                 uint16_t* __restrict__ out, int Hq, int Hkv, int g, int bl, int RG,
+                 int ps, int ps_shift, int max_pages, int num_pages, float scale_log2) {
+    __shared__ Bf16Tiles<D> sm;
+    constexpr int KK = D / 16;      // k-steps of the S^T product
+    constexpr int DT = D / 32;      // 32-wide d tiles of O^T
+    constexpr int NCH = D / 32;     // 16-byte loads per thread per key tile
+    constexpr int KCH = 4 * D;      // K chunks per tile (32 keys x D/8)
+
+    const int item = blockIdx.x;
+    if (item >= ws.counts[kCItems]) return;
+    const int32_t* it = ws.items + (size_t)item * 4;
+    const int u = it[kIUnit], kb = it[kIKb], ke = it[kIKe], slot = it[kISlot];
+    const int rg = u % RG;
+    const int c = (u / RG) % Hkv;
+    const int t = u / (RG * Hkv);
+    const int32_t* tile = pv.tiles + (size_t)t * kTileInts;
+    const int b = tile[kTB];
+    const int row0 = tile[kTRow0];
+    const int32_t* pt = page_table + (size_t)b * max_pages;
+
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 31;
+    const int h = lane >> 5;
+    const int r_local = wave * 32 + n;
+    const int r = rg * kRowsPerWg + r_local;
+    const bool row_ok = r < bl * g;
+    const int pos_local = row_ok ? r / g : 0;
+    const int hg = row_ok ? r % g : 0;
+    const size_t q_off = ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D;
+
+    bf16x8 qf[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        if (row_ok) {
+            qf[kk] = *reinterpret_cast<const bf16x8*>(q + q_off + kk * 16 + h * 8);
+        } else {
+            qf[kk] = bf16x8{};
+        }
+    }
+
+    floatx16 o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = floatx16{};
+    float m_run = -INFINITY;   // running max of scores, log2 domain
+    float l_part = 0.f;        // this lane's share of the softmax denominator
+
+    const int kt0 = kb / kKeyTile;
+    const int kt1 = (ke + kKeyTile - 1) / kKeyTile;
+
+    uint4 stage[NCH];
+    auto load_tile = [&](int kt) {
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            const int e = threadIdx.x + j * kAttnThreads;
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (e < KCH) {
+                const int key = e / (D / 8);
+                const int dc = e % (D / 8);
+                const int kg = kt * kKeyTile + key;
+                if (kg < ke) {
+                    const int page = pt[kg >> ps_shift];
+                    if (page >= 0 && page < num_pages) {
+                        const size_t off = (((size_t)page * Hkv + c) * ps + (kg & (ps - 1))) * D + dc * 8;
+                        val = *reinterpret_cast<const uint4*>(k_cache + off);
+                    } else if (dc == 0) {
+                        record_error(pv.hdr, b, FB_DERR_PAGE);
+                    }
+                }
+            } else {
+                const int e2 = e - KCH;
+                const int d = e2 >> 2;
+                const int kc = e2 & 3;
+                const int kg = kt * kKeyTile + kc * 8;
+                const int nvalid = ke - kg;
+                const int page = nvalid > 0 ? pt[kg >> ps_shift] : -1;
+                if (nvalid > 0 && page >= 0 && page < num_pages) {
+                    const size_t off = (((size_t)page * Hkv + c) * D + d) * ps + (kg & (ps - 1));
+                    val = *reinterpret_cast<const uint4*>(v_cache + off);
+                    if (nvalid < 8) {
+                        uint32_t w[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+                        for (int x = 0; x < 8; ++x) {
+                            if (x >= nvalid) w[x >> 1] &= (x & 1) ? 0x0000ffffu : 0xffff0000u;
+                        }
+                        val = make_uint4(w[0], w[1], w[2], w[3]);
+                    }
+                }
+            }
+            stage[j] = val;
+        }
+    };
+    auto store_tile = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            const int e = threadIdx.x + j * kAttnThreads;
+            if (e < KCH) {
+                const int key = e / (D / 8);
+                const int dc = e % (D / 8);
+                *reinterpret_cast<uint4*>(&sm.k[buf][key * Bf16Tiles<D>::kRowK + dc * 8]) = stage[j];
+            } else {
+                const int e2 = e - KCH;
+                const int d = e2 >> 2;
+                const int kc = e2 & 3;
+                *reinterpret_cast<uint4*>(&sm.v[buf][d * Bf16Tiles<D>::kRowV + kc * 8]) = stage[j];
+            }
+        }
+    };
+
+    const int krow = swap_bits23(n);
+    if (kt0 < kt1) {
+        load_tile(kt0);
+        store_tile(0);
+    }
+    __syncthreads();
+    for (int kt = kt0; kt < kt1; ++kt) {
+        const int buf = (kt - kt0) & 1;
+        const bool more = kt + 1 < kt1;
+        if (more) load_tile(kt + 1);
+
+        // S^T (32 keys x 32 rows) = K Q^T
+        floatx16 s = floatx16{};
+        const uint16_t* kbase = &sm.k[buf][krow * Bf16Tiles<D>::kRowK + h * 8];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbase + kk * 16);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
+        }
+        // Mask keys at or past ke (only the last tile can have any).
+        if (kt * kKeyTile + kKeyTile > ke) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = 16 * (i >> 3) + 8 * h + (i & 7);
+                if (kt * kKeyTile + key >= ke) s[i] = -INFINITY;
+            }
+        }
+        float mx = s[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[i]);
+        mx = wave_xor32_max(mx) * scale_log2;
+        const bool need = mx > m_run + kRescaleSlack;
+        if (__any(need)) {
+            const float m_new = need ? mx : m_run;
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
+            l_part *= alpha;
+            m_run = m_new;
+        }
+        bf16x8 pb[2];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[i], scale_log2, -m_run));
+            l_part += p;
+            pb[i >> 3][i & 7] = (__bf16)p;
+        }
+        // O^T (d x 32 rows) += V^T (d x 32 keys) P^T (32 keys x 32 rows)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const uint16_t* vbase = &sm.v[buf][(dt * 32 + n) * Bf16Tiles<D>::kRowV + h * 8];
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(vbase + tt * 16);
+                o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[tt], o[dt], 0, 0, 0);
+            }
+        }
+        if (more) store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    const float l = l_part + __shfl_xor(l_part, 32, 64);
+    const float inv_l = 1.0f / l;
+    if (slot < 0) {
+        if (!row_ok) return;
+        uint16_t* orow = out + q_off;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const int d0 = dt * 32 + grp * 8 + h * 4;
+                __bf16 v4[4];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) v4[x] = (__bf16)(o[dt][grp * 4 + x] * inv_l);
+                *reinterpret_cast<uint2*>(orow + d0) = *reinterpret_cast<const uint2*>(v4);
+            }
+        }
+    } else {
+        float* po = ws.part_o + ((size_t)slot * kRowsPerWg + r_local) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const int d0 = dt * 32 + grp * 8 + h * 4;
+                float4 v4 = make_float4(o[dt][grp * 4 + 0] * inv_l, o[dt][grp * 4 + 1] * inv_l,
+                                        o[dt][grp * 4 + 2] * inv_l, o[dt][grp * 4 + 3] * inv_l);
+                *reinterpret_cast<float4*>(po + d0) = v4;
+            }
+        }
+        if (h == 0) ws.part_lse[(size_t)slot * kRowsPerWg + r_local] = m_run + __log2f(l);
+    }
+}
+
+// ------------------------------------------------------------ combine -----
+template <typename T>
+__device__ inline void store_out(T* p, float v);
+template <>
+__device__ inline void store_out<uint16_t>(uint16_t* p, float v) {
+    __bf16 x = (__bf16)v;
+    *p = *reinterpret_cast<uint16_t*>(&x);
+}
+template <>
+__device__ inline void store_out<float>(float* p, float v) { *p = v; }
+
+template <typename T>
+__global__ void __launch_bounds__(kAttnThreads)
+combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
+               int g, int bl, int RG, int D) {
+    const int u = blockIdx.x;
+    if (u >= ws.counts[kCUnits]) return;
+    const int ns = ws.units[(size_t)u * 2 + kUSplits];
+    if (ns <= 1) return;
+    const int slot0 = ws.units[(size_t)u * 2 + kUSlot0];
+    const int rg = u % RG;
+    const int c = (u / RG) % Hkv;
+    const int t = u / (RG * Hkv);
+    const int row0 = pv.tiles[(size_t)t * kTileInts + kTRow0];
+    for (int e = threadIdx.x; e < kRowsPerWg * D; e += kAttnThreads) {
+        const int rl = e / D;
+        const int d = e % D;
+        const int r = rg * kRowsPerWg + rl;
+        if (r >= bl * g) break;
+        float mx = -INFINITY;
+        for (int k = 0; k < ns; ++k)
+            mx = fmaxf(mx, ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl]);
+        float num = 0.f, den = 0.f;
+        for (int k = 0; k < ns; ++k) {
+            const float wgt = __builtin_amdgcn_exp2f(
+                ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl] - mx);
+            num += wgt * ws.part_o[((size_t)(slot0 + k) * kRowsPerWg + rl) * D + d];
+            den += wgt;
+        }
+        const int pos_local = r / g, hg = r % g;
+        store_out<T>(out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d, num / den);
+    }
+}
+
+// ---------------------------------------------------------------- fp32 ----
+// One workgroup per (tile, query head); each wave walks its rows with an
+// online softmax over 64-key chunks, one key per lane.
+constexpr int kF32MaxD = 256;
+
+__global__ void __launch_bounds__(kAttnThreads)
+attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k_cache,
+                const float* __restrict__ v_cache, const int32_t* __restrict__ page_table,
+                PackView pv, float* __restrict__ out, int Hq, int Hkv, int D, int bl,
+                int ps, int max_pages, int num_pages, float sm_scale) {
+    const int t = blockIdx.x;
+    const int hq = blockIdx.y;
+    if (t >= pv.hdr[kHdrTiles]) return;
+    const int32_t* tile = pv.tiles + (size_t)t * kTileInts;
+    const int b = tile[kTB];
+    const int row0 = tile[kTRow0];
+    const int kv_len = tile[kTKvLen];
+    const int c = hq / (Hq / Hkv);
+    const int32_t* pt = page_table + (size_t)b * max_pages;
+    // Every page the tile reads must be valid, else the tile is skipped.
+    __shared__ int bad_page;
+    if (threadIdx.x == 0) bad_page = 0;
+    __syncthreads();
+    if ((long long)kv_len > (long long)max_pages * ps) {
+        if (threadIdx.x == 0) bad_page = 1;
+    } else {
+        for (int p = threadIdx.x; p * ps < kv_len; p += kAttnThreads) {
+            const int id = pt[p];
+            if (id < 0 || id >= num_pages) bad_page = 1;
+        }
+    }
+    __syncthreads();
+    if (bad_page) {
+        if (threadIdx.x == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
+        return;
+    }
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    constexpr int kAcc = kF32MaxD / 64;
+
+    for (int i = wave; i < bl; i += kAttnThreads / 64) {
+        const float* qrow = q + ((size_t)(row0 + i) * Hq + hq) * D;
+        float m = -INFINITY, l = 0.f;
+        float acc[kAcc];
+#pragma unroll
+        for (int j = 0; j < kAcc; ++j) acc[j] = 0.f;
+        for (int k0 = 0; k0 < kv_len; k0 += 64) {
+            const int key = k0 + lane;
+            float s = -INFINITY;
+            if (key < kv_len) {
+                const int page = pt[key / ps];
+                const float* krow = k_cache + (((size_t)page * Hkv + c) * ps + key % ps) * D;
+                float dot = 0.f;
+                for (int d = 0; d < D; ++d) dot = fmaf(qrow[d], krow[d], dot);
+                s = dot * sm_scale;
+            }
+            float cm = s;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
+            const float m_new = fmaxf(m, cm);
+            const float alpha = expf(m - m_new);
+            const float p = key < kv_len ? expf(s - m_new) : 0.f;
+            float ps_sum = p;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) ps_sum += __shfl_xor(ps_sum, off, 64);
+            l = l * alpha + ps_sum;
+#pragma unroll
+            for (int j = 0; j < kAcc; ++j) acc[j] *= alpha;
+            const int nk = min(64, kv_len - k0);
+            for (int jj = 0; jj < nk; ++jj) {
+                const float pj = __shfl(p, jj, 64);
+                const int kk = k0 + jj;
+                const int page = pt[kk / ps];
+                const float* vcol = v_cache + ((size_t)page * Hkv + c) * D * ps + kk % ps;
+#pragma unroll
+                for (int j = 0; j < kAcc; ++j) {
+                    const int d = lane + 64 * j;
+                    if (d < D) acc[j] = fmaf(pj, vcol[(size_t)d * ps], acc[j]);
+                }
+            }
+            m = m_new;
+        }
+        float* orow = out + ((size_t)(row0 + i) * Hq + hq) * D;
+#pragma unroll
+        for (int j = 0; j < kAcc; ++j) {
+            const int d = lane + 64 * j;
+            if (d < D) orow[d] = acc[j] / l;
+        }
+    }
+}
+
+}  // namespace
+
+AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
+                              int cu_count) {
+    AttnPlanSizes z{};
+    const int g = sh->Hq / sh->Hkv;
+    z.rows_per_unit = pack->bl * g;
+    z.row_groups = (z.rows_per_unit + kRowsPerWg - 1) / kRowsPerWg;
+    z.unit_cap = pack->tile_cap * sh->Hkv * z.row_groups;
+    z.target_items = 8 * (cu_count > 0 ? cu_count : 256);
+    z.item_cap = z.unit_cap + z.target_items;
+    z.slot_cap = 2 * z.target_items;
+    const size_t D = sh->head_dim;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t at = off;
+        off += (bytes + 255) & ~(size_t)255;
+        return at;
+    };
+    z.off_items = take((size_t)z.item_cap * 4 * sizeof(int32_t));
+    z.off_units = take((size_t)z.unit_cap * 2 * sizeof(int32_t));
+    z.off_counts = take(4 * sizeof(int32_t));
+    if (sh->dtype == FB_BF16) {
+        z.off_part_o = take((size_t)z.slot_cap * kRowsPerWg * D * sizeof(float));
+        z.off_part_lse = take((size_t)z.slot_cap * kRowsPerWg * sizeof(float));
+    } else {
+        z.off_part_o = z.off_part_lse = off;
+    }
+    z.total = off;
+    return z;
+}
+
+hipError_t launch_attention(const void* q, const void* k_cache,
+                            const void* v_cache, const int32_t* page_table,
+                            const fb_pack* pack, const fb_attn_shape* sh,
+                            void* out, void* wsp, const AttnPlanSizes& z,
+                            hipStream_t stream) {
+    PackView pv = pack_view(pack);
+    const int g = sh->Hq / sh->Hkv;
+    const float scale = sh->sm_scale > 0.f ? sh->sm_scale
+                                           : 1.0f / sqrtf((float)sh->head_dim);
+    if (sh->dtype == FB_F32) {
+        hipLaunchKernelGGL(attn_f32_kernel, dim3(pack->tile_cap, sh->Hq),
+                           dim3(kAttnThreads), 0, stream,
+                           static_cast<const float*>(q),
+                           static_cast<const float*>(k_cache),
+                           static_cast<const float*>(v_cache), page_table, pv,
+                           static_cast<float*>(out), sh->Hq, sh->Hkv,
+                           sh->head_dim, pack->bl, sh->page_size, sh->max_pages,
+                           sh->num_pages, scale);
+        return hipGetLastError();
+    }
+    char* base = static_cast<char*>(wsp);
+    AttnWs ws{reinterpret_cast<int32_t*>(base + z.off_items),
+              reinterpret_cast<int32_t*>(base + z.off_units),
+              reinterpret_cast<int32_t*>(base + z.off_counts),
+              reinterpret_cast<float*>(base + z.off_part_o),
+              reinterpret_cast<float*>(base + z.off_part_lse)};
+    const int fixed_chunk = sh->kv_split > 0 ? sh->kv_split / kKeyTile : 0;
+    const long long max_keys = (long long)sh->max_pages * sh->page_size;
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pv,
+                       ws, sh->Hkv, z.row_groups, z.item_cap, z.slot_cap,
+                       z.target_items, fixed_chunk, max_keys);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int shift = 0;
+    while ((1 << shift) < sh->page_size) ++shift;
+    const float scale_log2 = scale * kLog2e;
+    const uint16_t* qb = static_cast<const uint16_t*>(q);
+    const uint16_t* kc = static_cast<const uint16_t*>(k_cache);
+    const uint16_t* vc = static_cast<const uint16_t*>(v_cache);
+    uint16_t* ob = static_cast<uint16_t*>(out);
+    switch (sh->head_dim) {
+        case 32:
+            hipLaunchKernelGGL(attn_bf16_kernel<32>, dim3(z.item_cap), dim3(kAttnThreads),
+                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
+                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
+                               sh->max_pages, sh->num_pages, scale_log2);
+            break;
+        case 64:
+            hipLaunchKernelGGL(attn_bf16_kernel<64>, dim3(z.item_cap), dim3(kAttnThreads),
+                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
+                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
+                               sh->max_pages, sh->num_pages, scale_log2);
+            break;
+        default:
+            hipLaunchKernelGGL(attn_bf16_kernel<128>, dim3(z.item_cap), dim3(kAttnThreads),
+                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
+                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
+                               sh->max_pages, sh->num_pages, scale_log2);
+            break;
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.unit_cap), dim3(kAttnThreads),
+                       0, stream, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl,
+                       z.row_groups, sh->head_dim);
+    return hipGetLastError();
+}
+
+}  // namespace fb

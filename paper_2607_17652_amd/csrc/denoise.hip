@@ -1,0 +1,431 @@
+// Denoise update: vocab-wide reduction, joint M2T/T2T update (Eq. 1), block
+// readiness (Eq. 2), post-edit bookkeeping (Sec. 3.1), in-order retirement and
+// readiness-gated admission (Alg. 1, Eq. 3).
+//
+// vocab_pass_kernel   one workgroup per (live row, vocabulary partition):
+//                     streams the logits once in 16-byte loads and keeps, per
+//                     thread, (max, lowest index of the max, sum of
+//                     exp2(z*log2e - round(max*log2e))); wavefront butterfly
+//                     then LDS merge; one 16-byte partial per partition.
+// request_kernel      one workgroup per request: merges a row's partials in
+//                     partition order, applies Eq. 1, counts each live block,
+//                     then retires and admits on one thread.
+// Every reduction has a fixed order, so results are bit-reproducible.
+#include "internal.h"
+
+namespace fb {
+namespace {
+
+constexpr int kVocabThreads = 256;
+constexpr int kUpdThreads = 256;
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Running (max, index, scaled sum).  `s` is relative to mL = round(m*log2e).
+struct Top {
+    float m;
+    float mL;
+    float s;
+    int idx;
+};
+
+__device__ inline Top top_empty() { return Top{-INFINITY, -INFINITY, 0.f, 0x7fffffff}; }
+
+// The reference mL must be the rounded product everywhere it is used: with
+// contraction, `x - m*log2e` would become an fma on the exact product and
+// every merge would scale the sum by the product's rounding error.
+__device__ inline float scaled_ref(float m) {
+#pragma clang fp contract(off)
+    return m * kLog2e;
+}
+
+// Order-independent merge of two partial results (commutative bit for bit).
+__device__ inline Top top_merge(const Top& a, const Top& b) {
+#pragma clang fp contract(off)
+    if (a.m == -INFINITY) return b;
+    if (b.m == -INFINITY) return a;
+    Top r;
+    r.m = fmaxf(a.m, b.m);
+    r.mL = scaled_ref(r.m);
+    r.s = a.s * __builtin_amdgcn_exp2f(a.mL - r.mL) + b.s * __builtin_amdgcn_exp2f(b.mL - r.mL);
+    r.idx = a.m > b.m ? a.idx : (b.m > a.m ? b.idx : min(a.idx, b.idx));
+    return r;
+}
+
+// Fold n consecutive values starting at index v into t (values in index order).
+template <int N>
+__device__ inline void top_fold(Top& t, const float (&f)[N], int v) {
+    float vmax = f[0];
+#pragma unroll
+    for (int j = 1; j < N; ++j) vmax = fmaxf(vmax, f[j]);
+    if (vmax > t.m) {
+#pragma clang fp contract(off)
+        int j0 = N - 1;
+#pragma unroll
+        for (int j = N - 1; j >= 0; --j)
+            if (f[j] == vmax) j0 = j;
+        const float nmL = scaled_ref(vmax);
+        t.s *= __builtin_amdgcn_exp2f(t.mL - nmL);
+        t.m = vmax;
+        t.mL = nmL;
+        t.idx = v + j0;
+    }
+    float e[N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(f[j], kLog2e, -t.mL));
+#pragma unroll
+    for (int w = 1; w < N; w <<= 1)
+#pragma unroll
+        for (int j = 0; j + w < N; j += 2 * w) e[j] += e[j + w];
+    t.s += e[0];
+}
+
+template <typename T>
+struct VecTraits;
+template <>
+struct VecTraits<uint16_t> {   // bf16
+    static constexpr int N = 8;
+    __device__ static inline void unpack(const uint4& u, float (&f)[8]) {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f[2 * j] = __uint_as_float(w[j] << 16);
+            f[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+        }
+    }
+    __device__ static inline float scalar(const uint16_t* p) {
+        return __uint_as_float(((uint32_t)*p) << 16);
+    }
+};
+template <>
+struct VecTraits<float> {
+    static constexpr int N = 4;
+    __device__ static inline void unpack(const uint4& u, float (&f)[4]) {
+        f[0] = __uint_as_float(u.x);
+        f[1] = __uint_as_float(u.y);
+        f[2] = __uint_as_float(u.z);
+        f[3] = __uint_as_float(u.w);
+    }
+    __device__ static inline float scalar(const float* p) { return *p; }
+};
+
+template <typename T>
+__global__ void __launch_bounds__(kVocabThreads)
+vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
+                  PackView pv, float4* __restrict__ part) {
+    using VT = VecTraits<T>;
+    constexpr int N = VT::N;
+    constexpr int kBatch = 4;
+    const int row = blockIdx.x / nsplit;
+    const int k = blockIdx.x % nsplit;
+    if (pv.row_req[row] < 0) return;
+    const int v0 = k * chunk;
+    const int v1 = min(V, v0 + chunk);
+    const T* rp = logits + (size_t)row * V;
+    const int tid = threadIdx.x;
+
+    // Body [a, e) is 16-byte aligned in memory; head [v0, a) and tail [e, v1)
+    // are taken one element at a time by the first threads.
+    const size_t abs0 = (size_t)row * V + v0;
+    int a = v0 + (int)((N - (abs0 % N)) % N);
+    if (a > v1) a = v1;
+    int e = a + ((v1 - a) / N) * N;
+
+    Top t = top_empty();
+    if (tid < a - v0) {
+        float f[1] = {VT::scalar(rp + v0 + tid)};
+        top_fold<1>(t, f, v0 + tid);
+    }
+    const int stride = kVocabThreads * N;
+    for (int base = a + tid * N; base < e; base += kBatch * stride) {
+        uint4 raw[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int v = base + j * stride;
+            raw[j] = v < e ? *reinterpret_cast<const uint4*>(rp + v) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int v = base + j * stride;
+            if (v < e) {
+                float f[N];
+                VT::unpack(raw[j], f);
+                top_fold<N>(t, f, v);
+            }
+        }
+    }
+    if (tid < v1 - e) {
+        float f[1] = {VT::scalar(rp + e + tid)};
+        top_fold<1>(t, f, e + tid);
+    }
+
+    // Wavefront butterfly (every lane ends with the same value), then waves
+    // merged in order by thread 0.
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        Top o;
+        o.m = __shfl_xor(t.m, off, 64);
+        o.mL = __shfl_xor(t.mL, off, 64);
+        o.s = __shfl_xor(t.s, off, 64);
+        o.idx = __shfl_xor(t.idx, off, 64);
+        t = top_merge(t, o);
+    }
+    __shared__ Top wtop[kVocabThreads / 64];
+    if ((tid & 63) == 0) wtop[tid >> 6] = t;
+    __syncthreads();
+    if (tid == 0) {
+        Top r = wtop[0];
+        for (int w = 1; w < kVocabThreads / 64; ++w) r = top_merge(r, wtop[w]);
+        part[(size_t)row * nsplit + k] = make_float4(r.m, r.s, __int_as_float(r.idx), r.mL);
+    }
+}
+
+struct UpdParams {
+    double tau_mask, tau_edit, theta;
+    int mask_id, eos_id, S_pe, W;
+    unsigned flags;
+};
+
+enum RowFlag : uint8_t {
+    kMaskedBefore = 1,
+    kDecodable = 2,
+    kGamma = 4,
+    kWritten = 8,
+    kForceable = 16,
+};
+
+__global__ void __launch_bounds__(kUpdThreads)
+request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
+               int32_t* __restrict__ tokens, int T_max, float* __restrict__ conf_out,
+               int32_t* __restrict__ argmax_out, fb_req_state* __restrict__ st,
+               uint8_t* __restrict__ pe, uint8_t* __restrict__ fin, int n_max, int bl,
+               int W_max, UpdParams prm, fb_req_stats* __restrict__ stats) {
+    extern __shared__ unsigned char upd_smem[];
+    const int rows_cap = W_max * bl;
+    float* s_conf = reinterpret_cast<float*>(upd_smem);
+    int* s_xhat = reinterpret_cast<int*>(s_conf + rows_cap);
+    uint8_t* s_flag = reinterpret_cast<uint8_t*>(s_xhat + rows_cap);
+    __shared__ double s_rho[64];
+    __shared__ int s_m2t[64], s_t2t[64];
+
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int w = pv.req_w[b];
+    if (w < 0) {
+        if (tid == 0 && stats) {
+            fb_req_stats z{};
+            z.valid = 0;
+            z.rho_frontier = -1.0;
+            stats[b] = z;
+        }
+        return;
+    }
+    const fb_req_state s = st[b];
+    const int row0 = pv.req_row0[b];
+    const int nrows = w * bl;
+    const int o = s.gen_start + s.L * bl;
+    int32_t* tok = tokens + (size_t)b * T_max;
+
+    // ---- rows: merge partials, Eq. 1 ----------------------------------------
+    for (int i = tid; i < nrows; i += kUpdThreads) {
+        const int row = row0 + i;
+        const int pos = o + i;
+        const float4* pr = part + (size_t)row * nsplit;
+        float4 p0 = pr[0];
+        Top t{p0.x, p0.w, p0.y, __float_as_int(p0.z)};
+        for (int k = 1; k < nsplit; ++k) {
+            const float4 pk = pr[k];
+            t = top_merge(t, Top{pk.x, pk.w, pk.y, __float_as_int(pk.z)});
+        }
+        // s is relative to round(m*log2e); undo that rounding exactly.
+        const float resid = fmaf(t.m, kLog2e, -t.mL);
+        const float conf = 1.0f / (t.s * __builtin_amdgcn_exp2f(-resid));
+        const int xhat = t.idx;
+        const int x = tok[pos];
+        const bool masked = x == prm.mask_id;
+        const bool prompt = pos < s.prompt_len;
+        const double c = (double)conf;
+        const bool gamma = masked && c > prm.tau_mask && xhat != prm.mask_id;
+        const bool delta = ((prm.flags & FB_EDIT_MASKED) || !masked) && !prompt &&
+                           xhat != x && c > prm.tau_edit && xhat != prm.mask_id;
+        uint8_t f = 0;
+        if (masked) f |= kMaskedBefore;
+        if (masked && c >= prm.tau_mask) f |= kDecodable;
+        if (gamma) f |= kGamma;
+        if (gamma || delta) {
+            f |= kWritten;
+            tok[pos] = xhat;
+        }
+        if (masked && xhat != prm.mask_id) f |= kForceable;
+        conf_out[row] = conf;
+        argmax_out[row] = xhat;
+        s_conf[i] = conf;
+        s_xhat[i] = xhat;
+        s_flag[i] = f;
+    }
+    __syncthreads();
+
+    // ---- blocks: one wavefront per live block --------------------------------
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    for (int sl = wave; sl < w; sl += kUpdThreads / 64) {
+        int m_before = 0, dec = 0, n_gamma = 0, u = 0, wr_masked = 0;
+        float best_c = -1.f;
+        int best_i = 0x7fffffff;
+        for (int i = sl * bl + lane; i < (sl + 1) * bl; i += 64) {
+            const uint8_t f = s_flag[i];
+            m_before += (f & kMaskedBefore) ? 1 : 0;
+            dec += (f & kDecodable) ? 1 : 0;
+            n_gamma += (f & kGamma) ? 1 : 0;
+            u += (f & kWritten) ? 1 : 0;
+            wr_masked += ((f & kWritten) && (f & kMaskedBefore)) ? 1 : 0;
+            if ((f & kForceable) && s_conf[i] > best_c) {
+                best_c = s_conf[i];
+                best_i = i;
+            }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            m_before += __shfl_xor(m_before, off, 64);
+            dec += __shfl_xor(dec, off, 64);
+            n_gamma += __shfl_xor(n_gamma, off, 64);
+            u += __shfl_xor(u, off, 64);
+            wr_masked += __shfl_xor(wr_masked, off, 64);
+            const float oc = __shfl_xor(best_c, off, 64);
+            const int oi = __shfl_xor(best_i, off, 64);
+            if (oc > best_c || (oc == best_c && oi < best_i)) {
+                best_c = oc;
+                best_i = oi;
+            }
+        }
+        if (lane == 0) {
+            if ((prm.flags & FB_FORCE_PROGRESS) && m_before > 0 && n_gamma == 0 &&
+                best_i != 0x7fffffff) {
+                tok[o + best_i] = s_xhat[best_i];
+                u += 1;
+                wr_masked += 1;
+            }
+            const int m_after = m_before - wr_masked;
+            const int g = s.L + sl;
+            uint8_t* pe_g = pe + (size_t)b * n_max + g;
+            uint8_t* fin_g = fin + (size_t)b * n_max + g;
+            if (m_before == 0) {
+                const int npe = min(255, (int)*pe_g + 1);
+                *pe_g = (uint8_t)npe;
+                if (u == 0 || npe >= prm.S_pe) *fin_g = 1;
+            } else if (m_after == 0 && prm.S_pe == 0) {
+                *fin_g = 1;
+            }
+            s_rho[sl] = m_before == 0 ? 1.0 : (double)dec / (double)m_before;
+            s_m2t[sl] = wr_masked;
+            s_t2t[sl] = u - wr_masked;
+        }
+    }
+    __syncthreads();
+
+    // ---- retire, then admit (Alg. 1) -----------------------------------------
+    if (tid != 0) return;
+    fb_req_stats rs{};
+    rs.valid = 1;
+    rs.rho_frontier = w > 0 ? s_rho[w - 1] : -1.0;
+    for (int sl = 0; sl < w; ++sl) {
+        rs.m2t += s_m2t[sl];
+        rs.t2t += s_t2t[sl];
+    }
+    fb_req_state ns = s;
+    if (ns.active) {
+        const uint8_t* fin_b = fin + (size_t)b * n_max;
+        while (ns.L < ns.R && fin_b[ns.L]) {
+            const int g = ns.L;
+            ns.L += 1;
+            rs.committed += 1;
+            if (prm.eos_id >= 0) {
+                const int lo = ns.gen_start + g * bl;
+                bool hit = false;
+                for (int i = 0; i < bl; ++i) hit |= tok[lo + i] == prm.eos_id;
+                if (hit) {
+                    ns.active = 0;
+                    ns.eos_hit = 1;
+                    rs.eos = 1;
+                    rs.done = 1;
+                    break;
+                }
+            }
+        }
+        if (ns.active && ns.L >= ns.n_blocks) {
+            ns.active = 0;
+            rs.done = 1;
+        }
+        if (ns.active) {
+            const int L0 = s.L, R0 = s.R;
+            auto admit = [&]() {
+                pe[(size_t)b * n_max + ns.R] = 0;
+                fin[(size_t)b * n_max + ns.R] = 0;
+                ns.R += 1;
+                rs.spawned += 1;
+            };
+            if (ns.L == ns.R && ns.R < ns.n_blocks) admit();
+            while (ns.R - ns.L < prm.W && ns.R < ns.n_blocks) {
+                const int g = ns.R - 1;
+                double rho;
+                if (g < ns.L) rho = 1.0;                      // committed
+                else if (g >= L0 && g < R0) rho = s_rho[g - L0];  // live this step
+                else rho = 0.0;                               // admitted this step
+                if (!(rho >= prm.theta)) break;
+                admit();
+            }
+        }
+    }
+    st[b] = ns;
+    if (stats) stats[b] = rs;
+}
+
+}  // namespace
+
+UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count) {
+    UpdateSizes z{};
+    const int target = 8 * (cu_count > 0 ? cu_count : 256);
+    const int min_chunk = 2048;
+    int ns = (target + pack->row_cap - 1) / pack->row_cap;
+    const int max_ns = V / min_chunk > 1 ? V / min_chunk : 1;
+    if (ns > max_ns) ns = max_ns;
+    if (ns > 64) ns = 64;
+    if (ns < 1) ns = 1;
+    int chunk = (V + ns - 1) / ns;
+    chunk = (chunk + 7) / 8 * 8;
+    z.nsplit = (V + chunk - 1) / chunk;
+    z.chunk = chunk;
+    z.total = (size_t)pack->row_cap * z.nsplit * sizeof(float4);
+    return z;
+}
+
+hipError_t launch_update(const void* logits, int V, int dtype, int32_t* tokens,
+                         int T_max, float* conf, int32_t* argmax,
+                         fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
+                         const fb_pack* pack, const fb_update_params* p,
+                         fb_req_stats* stats, void* ws, const UpdateSizes& z,
+                         hipStream_t stream) {
+    PackView pv = pack_view(pack);
+    float4* part = static_cast<float4*>(ws);
+    const dim3 grid((unsigned)pack->row_cap * (unsigned)z.nsplit);
+    if (dtype == FB_BF16) {
+        hipLaunchKernelGGL(vocab_pass_kernel<uint16_t>, grid, dim3(kVocabThreads), 0,
+                           stream, static_cast<const uint16_t*>(logits), V, z.nsplit,
+                           z.chunk, pv, part);
+    } else {
+        hipLaunchKernelGGL(vocab_pass_kernel<float>, grid, dim3(kVocabThreads), 0,
+                           stream, static_cast<const float*>(logits), V, z.nsplit,
+                           z.chunk, pv, part);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    UpdParams prm{p->tau_mask, p->tau_edit, p->theta_spawn, p->mask_id,
+                  p->eos_id,   p->S_pe,     p->W,           p->flags};
+    const size_t rows_cap = (size_t)pack->W_max * pack->bl;
+    const size_t smem = rows_cap * (sizeof(float) + sizeof(int) + 1);
+    hipLaunchKernelGGL(request_kernel, dim3(pack->B), dim3(kUpdThreads), smem, stream,
+                       part, z.nsplit, pv, tokens, T_max, conf, argmax, st, pe, fin,
+                       n_max, pack->bl, pack->W_max, prm, stats);
+    return hipGetLastError();
+}
+
+}  // namespace fb

@@ -1,0 +1,94 @@
+// Window KV write-back, Eq. 6 (Sec. 4.2, "KV retrieval and write-back"):
+// the fresh K/V of each live block lands at its absolute positions of the
+// paged caches.  One workgroup per (tile, KV head).  K rows are copied in
+// 16-byte vectors; V is staged through LDS and written key-innermost
+// ([page][head][d][slot]) with consecutive lanes on consecutive slots.
+#include "internal.h"
+
+namespace fb {
+namespace {
+
+constexpr int kKvThreads = 256;
+
+template <typename T>
+__global__ void __launch_bounds__(kKvThreads)
+write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
+                T* __restrict__ k_cache, T* __restrict__ v_cache,
+                const int32_t* __restrict__ page_table, PackView pv, int Hkv,
+                int D, int bl, int ps, int max_pages, int num_pages) {
+    extern __shared__ unsigned char kv_smem[];
+    T* vs = reinterpret_cast<T*>(kv_smem);   // [bl][D]
+    const int t = blockIdx.x;
+    const int c = blockIdx.y;
+    if (t >= pv.hdr[kHdrTiles]) return;
+    const int32_t* tile = pv.tiles + (size_t)t * kTileInts;
+    const int b = tile[kTB];
+    const int row0 = tile[kTRow0];
+    const int pos0 = tile[kTPos0];
+    const int32_t* pt = page_table + (size_t)b * max_pages;
+    constexpr int VEC = 16 / sizeof(T);
+    const int dch = D / VEC;
+
+    // K: straight 16-byte copies; V: rows into LDS.
+    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
+        const int i = e / dch;
+        const int dc = e % dch;
+        const int pos = pos0 + i;
+        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
+        const uint4 vv = *reinterpret_cast<const uint4*>(v_new + src);
+        *reinterpret_cast<uint4*>(vs + (size_t)i * D + dc * VEC) = vv;
+        const int pidx = pos / ps;
+        const int page = pidx < max_pages ? pt[pidx] : -1;
+        if (page < 0 || page >= num_pages) {
+            if (dc == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
+            continue;
+        }
+        const size_t dst = (((size_t)page * Hkv + c) * ps + (pos % ps)) * D +
+                           (size_t)dc * VEC;
+        *reinterpret_cast<uint4*>(k_cache + dst) =
+            *reinterpret_cast<const uint4*>(k_new + src);
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < bl * D; e += kKvThreads) {
+        const int d = e / bl;
+        const int i = e % bl;
+        const int pos = pos0 + i;
+        const int pidx = pos / ps;
+        const int page = pidx < max_pages ? pt[pidx] : -1;
+        if (page < 0 || page >= num_pages) continue;
+        v_cache[(((size_t)page * Hkv + c) * D + d) * ps + (pos % ps)] =
+            vs[(size_t)i * D + d];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_write_kv(const void* k_new, const void* v_new, void* k_cache,
+                           void* v_cache, const int32_t* page_table,
+                           const fb_pack* pack, const fb_attn_shape* sh,
+                           hipStream_t stream) {
+    PackView pv = pack_view(pack);
+    const dim3 grid(pack->tile_cap, sh->Hkv);
+    if (sh->dtype == FB_BF16) {
+        const size_t smem = (size_t)pack->bl * sh->head_dim * 2;
+        hipLaunchKernelGGL(write_kv_kernel<uint16_t>, grid, dim3(kKvThreads),
+                           smem, stream, static_cast<const uint16_t*>(k_new),
+                           static_cast<const uint16_t*>(v_new),
+                           static_cast<uint16_t*>(k_cache),
+                           static_cast<uint16_t*>(v_cache), page_table, pv,
+                           sh->Hkv, sh->head_dim, pack->bl, sh->page_size,
+                           sh->max_pages, sh->num_pages);
+    } else {
+        const size_t smem = (size_t)pack->bl * sh->head_dim * 4;
+        hipLaunchKernelGGL(write_kv_kernel<float>, grid, dim3(kKvThreads), smem,
+                           stream, static_cast<const float*>(k_new),
+                           static_cast<const float*>(v_new),
+                           static_cast<float*>(k_cache),
+                           static_cast<float*>(v_cache), page_table, pv, sh->Hkv,
+                           sh->head_dim, pack->bl, sh->page_size, sh->max_pages,
+                           sh->num_pages);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace fb

@@ -1,0 +1,140 @@
+// Heterogeneous Wavefront Packing, Eq. 4 (Sec. 4.2): one workgroup turns the
+// per-request wavefront states into the packed batch -- a compact list of
+// live-block tiles plus per-row request / position / token maps.
+//
+// Phase 1 validates every request and computes w_b; a block-wide exclusive
+// scan of w_b gives each request its first tile (and, in the ragged layout,
+// its first packed row).  Phase 2 writes every one of the row_cap row-map
+// entries exactly once, live or not, so the output is fully defined without
+// a separate clearing pass.
+#include "internal.h"
+
+namespace fb {
+namespace {
+
+constexpr int kPackThreads = 1024;
+constexpr int kPackWaves = kPackThreads / 64;
+
+// Exclusive scan of one int per thread across the workgroup; also returns the
+// total.  `lds` holds kPackWaves + 1 ints.
+__device__ int workgroup_exclusive_scan(int v, int* lds, int* total) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) lds[wave] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int w = 0; w < kPackWaves; ++w) {
+            int t = lds[w];
+            lds[w] = acc;
+            acc += t;
+        }
+        lds[kPackWaves] = acc;
+    }
+    __syncthreads();
+    int excl = lds[wave] + x - v;
+    *total = lds[kPackWaves];
+    __syncthreads();
+    return excl;
+}
+
+__global__ void __launch_bounds__(kPackThreads)
+pack_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tokens,
+            int B, int W_max, int bl, int layout, int n_max, int T_max,
+            PackView pv, int row_cap) {
+    __shared__ int scan_lds[kPackWaves + 1];
+    const int tid = threadIdx.x;
+    if (tid == 0) pv.hdr[kHdrStatus] = FB_PACK_STATUS_NONE;
+    __syncthreads();
+
+    // ---- phase 1: validate, scan w_b, write per-request fields and tiles --
+    int tiles_before = 0;
+    for (int base = 0; base < B; base += kPackThreads) {
+        const int b = base + tid;
+        int w = 0;
+        bool bad = false;
+        fb_req_state s{};
+        if (b < B) {
+            s = st[b];
+            if (s.active) {
+                const long long end = (long long)s.gen_start + (long long)s.n_blocks * bl;
+                const bool ok = s.L >= 0 && s.L <= s.R && s.R <= s.n_blocks &&
+                                s.n_blocks <= n_max && s.R - s.L <= W_max &&
+                                s.gen_start >= 0 && end <= (long long)T_max;
+                if (ok) w = s.R - s.L;
+                else bad = true;
+            }
+        }
+        int total;
+        const int excl = workgroup_exclusive_scan(w, scan_lds, &total);
+        if (b < B) {
+            const int tile0 = tiles_before + excl;
+            const int row0 = (layout == FB_PADDED) ? b * W_max * bl : tile0 * bl;
+            pv.req_w[b] = bad ? -1 : w;
+            pv.req_row0[b] = row0;
+            if (bad) record_error(pv.hdr, b, FB_DERR_STATE);
+            const int o = s.gen_start + s.L * bl;
+            for (int sl = 0; sl < w; ++sl) {
+                int32_t* t = pv.tiles + (size_t)(tile0 + sl) * kTileInts;
+                t[kTB] = b;
+                t[kTS] = sl;
+                t[kTG] = s.L + sl;
+                t[kTRow0] = row0 + sl * bl;
+                t[kTPos0] = o + sl * bl;
+                t[kTO] = o;
+                t[kTKvLen] = o + (sl + 1) * bl;
+                t[kTW] = w;
+            }
+        }
+        tiles_before += total;
+    }
+    const int n_tiles = tiles_before;
+    const int n_rows = n_tiles * bl;
+    __syncthreads();
+
+    // ---- phase 2: every row-map entry, written once ------------------------
+    const int q = W_max * bl;
+    for (int r = tid; r < row_cap; r += kPackThreads) {
+        int b = -1, pos = -1;
+        if (layout == FB_PADDED) {
+            const int rb = r / q;
+            const int slot = (r % q) / bl;
+            const int w = pv.req_w[rb];
+            if (slot < w) {
+                const fb_req_state s = st[rb];
+                b = rb;
+                pos = s.gen_start + s.L * bl + (r % q);
+            }
+        } else if (r < n_rows) {
+            const int32_t* t = pv.tiles + (size_t)(r / bl) * kTileInts;
+            b = t[kTB];
+            pos = t[kTPos0] + (r % bl);
+        }
+        pv.row_req[r] = b;
+        pv.row_pos[r] = pos;
+        pv.row_tok[r] = (b >= 0 && tokens) ? tokens[(size_t)b * T_max + pos] : -1;
+    }
+    if (tid == 0) {
+        pv.hdr[kHdrRows] = n_rows;
+        pv.hdr[kHdrTiles] = n_tiles;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_pack(const fb_req_state* st, const int32_t* tokens, int n_max,
+                       int T_max, const fb_pack* pack, hipStream_t stream) {
+    PackView pv = pack_view(pack);
+    hipLaunchKernelGGL(pack_kernel, dim3(1), dim3(kPackThreads), 0, stream, st,
+                       tokens, pack->B, pack->W_max, pack->bl, pack->layout,
+                       n_max, T_max, pv, pack->row_cap);
+    return hipGetLastError();
+}
+
+}  // namespace fb

@@ -31,7 +31,7 @@ f ~ U[0,1] with Bernoulli(f) rows for hetero64/serve256.  Mask-free live
 blocks carry pe ~ U{0..S_pe-1}; mask-free blocks that are not leftmost are
 finished with probability 1/2 (so several blocks can retire in one step).
 """
-from dataclasses import dataclass, field, replace
+from dataclasses import dataclass, replace
 
 import numpy as np
 
@@ -64,7 +64,7 @@ class Workload:
     theta: float = 0.5
     eos_id: int = -1
     W: int = 0                   # admission cap; 0 means W_max
-    extra: dict = field(default_factory=dict)
+    prefix_jitter: int = 0       # adds U{0..jitter} to each prefix (unaligned)
 
     @property
     def mask_id(self):
@@ -132,8 +132,10 @@ def _draw_prefixes(wl, rng):
         o = np.exp(rng.uniform(lo, hi, size=wl.B)).astype(np.int64)
     else:
         raise ValueError(kind)
-    o = (o // wl.bl) * wl.bl
-    return np.maximum(o, wl.bl)
+    o = np.maximum((o // wl.bl) * wl.bl, wl.bl)
+    if wl.prefix_jitter:
+        o = o + rng.integers(0, wl.prefix_jitter + 1, size=wl.B)
+    return o
 
 
 def _draw_windows(wl, rng):
@@ -158,8 +160,8 @@ def make_host_state(wl, seed=0):
     B, bl, n, M = wl.B, wl.bl, wl.n_blocks, wl.mask_id
     o = _draw_prefixes(wl, rng)
     w = _draw_windows(wl, rng)
-    L = np.array([rng.integers(0, min(ob // bl, n - wl.W_max) + 1) for ob in o],
-                 dtype=np.int64)
+    L = np.array([rng.integers(0, max(0, min(ob // bl, n - wl.W_max)) + 1)
+                  for ob in o], dtype=np.int64)
     gen_start = o - L * bl
     R = L + w
     T_need = gen_start + n * bl

@@ -1,0 +1,128 @@
+"""The C ABI library loads, exports every function include/flowblock.h
+declares, and rejects bad host-visible arguments before touching a GPU.
+CPU only: nothing here launches a kernel."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_17652_amd import binding as fb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flowblock.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(fb_\w+)\s*\(", src, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fb.LIB_PATH):
+        from paper_2607_17652_amd import build
+        build.build()
+    return fb.lib()
+
+
+def test_header_declares_the_bound_functions():
+    assert declared_functions() == sorted(fb.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", fb.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\b(fb_\w+)\b", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_version_and_sizes(lib):
+    assert fb.fb_version().startswith("flowblock")
+    assert fb.fb_pack_bytes(0, 1, 1) == 0
+    off = fb.fb_pack_get_offsets(3, 2, 4)
+    assert off["header"] == 0 and off["tiles"] == 64
+    assert off["req_w"] == 64 + 6 * 8 * 4
+    assert off["row_tok"] + 3 * 2 * 4 * 4 == off["total"] == fb.fb_pack_bytes(3, 2, 4)
+
+
+def test_struct_sizes_match_header():
+    assert ctypes.sizeof(fb.fb_pack) == 32
+    assert ctypes.sizeof(fb.fb_attn_shape) == 48
+    assert ctypes.sizeof(fb.fb_update_params) == 56
+    assert fb.REQ_STATE_DTYPE.itemsize == 32
+    assert fb.REQ_STATS_DTYPE.itemsize == 40
+
+
+def _init(lib, buf, nbytes, B, W, bl, layout):
+    h = fb.fb_pack()
+    rc = lib.fb_pack_init(ctypes.byref(h), buf, nbytes, B, W, bl, layout)
+    return rc, h
+
+
+def test_pack_init_validation(lib):
+    fake = ctypes.c_void_p(0x10000)     # never dereferenced by fb_pack_init
+    need = fb.fb_pack_bytes(4, 2, 8)
+    assert _init(lib, fake, need, 4, 2, 8, fb.FB_RAGGED)[0] == fb.FB_OK
+    assert _init(lib, None, need, 4, 2, 8, fb.FB_RAGGED)[0] == fb.FB_E_INVAL
+    assert _init(lib, fake, need - 1, 4, 2, 8, fb.FB_RAGGED)[0] == fb.FB_E_WORKSPACE
+    assert _init(lib, fake, need, 0, 2, 8, fb.FB_RAGGED)[0] == fb.FB_E_INVAL
+    assert _init(lib, fake, need, 4, 2, 8, 7)[0] == fb.FB_E_INVAL
+    assert _init(lib, ctypes.c_void_p(0x10004), need, 4, 2, 8, 0)[0] == fb.FB_E_INVAL
+    assert _init(lib, fake, 10**12, 4, 65, 8, 0)[0] == fb.FB_E_UNSUPPORTED
+    assert "W_max" in fb.fb_last_error()
+
+
+def test_calls_reject_bad_arguments_before_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    rc, h = _init(lib, fake, fb.fb_pack_bytes(2, 2, 32), 2, 2, 32, fb.FB_RAGGED)
+    assert rc == fb.FB_OK
+    sh = fb.make_shape(8, 3, 128, fb.FB_BF16, 32, 4, 8)         # 8 % 3 != 0
+    rc = lib.fb_wavefront_attention(fake, fake, fake, fake, ctypes.byref(h),
+                                    ctypes.byref(sh), fake, fake, 1 << 30, None)
+    assert rc == fb.FB_E_INVAL
+    sh = fb.make_shape(8, 4, 96, fb.FB_BF16, 32, 4, 8)          # head_dim 96
+    rc = lib.fb_write_window_kv(fake, fake, fake, fake, fake, ctypes.byref(h),
+                                ctypes.byref(sh), None)
+    assert rc == fb.FB_E_UNSUPPORTED
+    sh = fb.make_shape(8, 4, 128, fb.FB_BF16, 24, 4, 8)         # page 24
+    rc = lib.fb_write_window_kv(fake, fake, fake, fake, fake, ctypes.byref(h),
+                                ctypes.byref(sh), None)
+    assert rc == fb.FB_E_INVAL
+    sh = fb.make_shape(8, 4, 128, fb.FB_BF16, 4, 4, 8)          # bf16 page 4
+    rc = lib.fb_write_window_kv(fake, fake, fake, fake, fake, ctypes.byref(h),
+                                ctypes.byref(sh), None)
+    assert rc == fb.FB_E_UNSUPPORTED
+    sh = fb.make_shape(8, 4, 128, fb.FB_BF16, 32, 4, 8, kv_split=100)
+    rc = lib.fb_write_window_kv(fake, fake, fake, fake, fake, ctypes.byref(h),
+                                ctypes.byref(sh), None)
+    assert rc == fb.FB_E_INVAL
+    rc = lib.fb_write_window_kv(None, fake, fake, fake, fake, ctypes.byref(h),
+                                ctypes.byref(fb.make_shape(8, 4, 128, fb.FB_BF16, 32,
+                                                           4, 8)), None)
+    assert rc == fb.FB_E_INVAL
+    prm = fb.make_params(0.9, 0.8, 0.5, 99, -1, 2, 3)            # W > W_max
+    rc = lib.fb_denoise_update(fake, 100, fb.FB_BF16, fake, 64, fake, fake, fake,
+                               fake, fake, 4, ctypes.byref(h), ctypes.byref(prm),
+                               None, fake, 1 << 30, None)
+    assert rc == fb.FB_E_INVAL
+    prm = fb.make_params(0.9, 0.8, 0.5, 100, -1, 2, 2)           # mask_id == V
+    rc = lib.fb_denoise_update(fake, 100, fb.FB_BF16, fake, 64, fake, fake, fake,
+                               fake, fake, 4, ctypes.byref(h), ctypes.byref(prm),
+                               None, fake, 1 << 30, None)
+    assert rc == fb.FB_E_INVAL
+    prm = fb.make_params(0.9, 0.8, 0.5, 99, -1, 2, 2)
+    prm.flags = 0x80
+    rc = lib.fb_denoise_update(fake, 100, fb.FB_BF16, fake, 64, fake, fake, fake,
+                               fake, fake, 4, ctypes.byref(h), ctypes.byref(prm),
+                               None, fake, 1 << 30, None)
+    assert rc == fb.FB_E_INVAL
+    rc = lib.fb_pack_wavefronts(None, None, 4, 64, ctypes.byref(h), None)
+    assert rc == fb.FB_E_INVAL
+    bad = fb.fb_pack()
+    rc = lib.fb_pack_wavefronts(fake, None, 4, 64, ctypes.byref(bad), None)
+    assert rc == fb.FB_E_INVAL

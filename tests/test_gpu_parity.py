@@ -1,0 +1,313 @@
+"""GPU parity of the HIP wavefront step against the fp64 oracle, through the
+C ABI.  Bit-exact: packing, token ids, argmax, per-block pe/fin, request
+state and statistics (requests holding a confidence within 1e-5 of a
+threshold are counted and reported instead).  Attention within max-abs 1e-2
+(bf16) / 1e-5 (fp32); confidences within 5e-6 of the fp64 value."""
+import numpy as np
+import pytest
+import torch
+
+from harness import (OracleCase, compare_case, compare_pack, gpu_results, log,
+                     setup)
+from paper_2607_17652_amd import binding as fb
+
+pytestmark = pytest.mark.gpu
+
+
+def run_and_compare(name, reqs=None, seed=0, host_edit=None, kv_split=0,
+                    check_pack=True, **overrides):
+    wl, host, t, step = setup(name, seed, host_edit=host_edit, kv_split=kv_split,
+                              **overrides)
+    if reqs is None:
+        reqs = list(range(wl.B))
+    log(f"[parity] workload={name} seed={seed} overrides={overrides} "
+        f"B={wl.B} rows={wl.row_cap} reqs={len(reqs)}")
+    case = OracleCase(wl, host, t, reqs, step.page_table)
+    step.run()
+    torch.cuda.synchronize()
+    g = gpu_results(step)
+    if check_pack:
+        compare_pack(wl, host, g, host["tokens"])
+    case.run(wl.params())
+    summary = compare_case(wl, case, g, step)
+    log(f"[parity] {name}: rows={summary['rows']} attn_max_err="
+        f"{summary['attn_max_err']:.3e} band_requests={summary['band_requests']}")
+    return wl, host, step, g, case, summary
+
+
+def test_tiny_fp32_full():
+    run_and_compare("tiny")
+
+
+def test_single_request_bf16_full():
+    run_and_compare("single")
+
+
+def test_hetero64_padded_full():
+    run_and_compare("hetero64")
+
+
+def test_long8_sampled_requests():
+    """Long prefixes (16K-32K keys) exercise split-KV and the combine."""
+    run_and_compare("long8", reqs=[0, 5])
+
+
+def test_serve256_sampled_requests():
+    rng = np.random.default_rng(7)
+    reqs = sorted(rng.choice(256, size=12, replace=False).tolist())
+    run_and_compare("serve256", reqs=reqs)
+
+
+@pytest.mark.parametrize("overrides", [
+    dict(prefix_jitter=37),                         # unaligned prefixes: partial key tiles
+    dict(page_size=16),
+    dict(page_size=64),
+    dict(d=64, Hq=8, Hkv=8),                        # no GQA
+    dict(d=32, Hq=16, Hkv=2),                       # group of 8
+    dict(bl=16, page_size=16, W_max=5, window=("fixed", 5)),
+    dict(V=1001, prefix_jitter=5),                  # unaligned logit rows
+    dict(B=5, layout="padded", window=("uniform", 1, 3)),
+])
+def test_shape_variants(overrides):
+    run_and_compare("single", **overrides)
+
+
+def test_fp32_bigger_shapes():
+    run_and_compare("single", dtype="f32", B=3, prefix=("uniform", 40, 300),
+                    window=("uniform", 1, 3), V=5003, prefix_jitter=9)
+
+
+def test_explicit_kv_split_matches_oracle():
+    run_and_compare("hetero64", reqs=list(range(0, 64, 7)), kv_split=256)
+
+
+def test_repeat_is_bit_identical():
+    wl, host, t, step = setup("hetero64", seed=3)
+    log("[parity] repeat hetero64 seed=3")
+    snap = {k: v.clone() for k, v in dict(st=step.st, tokens=step.tokens,
+                                          pe=step.pe, fin=step.fin).items()}
+    step.run()
+    torch.cuda.synchronize()
+    out1, conf1, tok1 = step.out.clone(), step.conf.clone(), step.tokens.clone()
+    for k, v in snap.items():
+        getattr(step, k).copy_(v)
+    step.run()
+    torch.cuda.synchronize()
+    assert torch.equal(out1, step.out)
+    assert torch.equal(conf1, step.conf)
+    assert torch.equal(tok1, step.tokens)
+
+
+def test_ragged_and_padded_agree_bitwise():
+    """The same per-position inputs packed ragged and padded give bit-identical
+    per-position outputs and identical request state."""
+    from oracle import pack as opack      # row placement of the inputs only
+    from paper_2607_17652_amd import synth
+    from paper_2607_17652_amd.runner import WavefrontStep
+    wl, host, t, step = setup("hetero64", seed=4)          # padded
+    wl_r = synth.workload("hetero64", layout="ragged")
+    log("[parity] ragged vs padded hetero64 seed=4")
+    pp = opack.pack_wavefronts(host["state"], wl.W_max, wl.bl, "padded")
+    pr = opack.pack_wavefronts(host["state"], wl.W_max, wl.bl, "ragged")
+    key_r = {(b, p): r for r, (b, p) in enumerate(zip(pr["row_req"], pr["row_pos"]))
+             if b >= 0}
+    rows_p = [r for r in range(pp["cap"]) if pp["row_req"][r] >= 0]
+    rows_r = [key_r[(pp["row_req"][r], pp["row_pos"][r])] for r in rows_p]
+    ip = torch.tensor(rows_p, device="cuda")
+    ir = torch.tensor(rows_r, device="cuda")
+    t2 = dict(t)
+    for k in ("q", "k_new", "v_new", "logits"):
+        t2[k] = torch.zeros_like(t[k])
+        t2[k][ir] = t[k][ip]
+    step2 = WavefrontStep(wl_r, host, t2)
+    step.run()
+    step2.run()
+    torch.cuda.synchronize()
+    assert torch.equal(step.out[ip], step2.out[ir])
+    assert torch.equal(step.conf[ip], step2.conf[ir])
+    assert torch.equal(step.argmax[ip], step2.argmax[ir])
+    for k in ("tokens", "st", "pe", "fin"):
+        assert torch.equal(getattr(step, k), getattr(step2, k)), k
+
+
+def test_later_blocks_do_not_change_earlier_outputs():
+    """Sec. 4.1: perturbing the fresh K/V of window slots > s leaves every
+    output of slot s bit-identical."""
+    wl, host, t, step = setup("long8", seed=1, prefix=("uniform", 1000, 3000))
+    log("[parity] perturbation long8-short")
+    snap = {k: v.clone() for k, v in dict(k_cache=t["k_cache"],
+                                          v_cache=t["v_cache"]).items()}
+    step.pack_step()
+    step.kv_step()
+    step.attention_step()
+    torch.cuda.synchronize()
+    base = step.out.clone()
+    view = step.pack.view()
+    tiles = view["tiles"].cpu().numpy()
+    n_tiles = int(view["header"][1])
+    for k, v in snap.items():
+        t[k].copy_(v)
+    for i in range(n_tiles):
+        b, s, row0 = tiles[i, 0], tiles[i, 1], tiles[i, 3]
+        if s >= 1:
+            t["k_new"][row0:row0 + wl.bl] += 3.0
+            t["v_new"][row0:row0 + wl.bl] -= 2.0
+    step.pack_step()
+    step.kv_step()
+    step.attention_step()
+    torch.cuda.synchronize()
+    for i in range(n_tiles):
+        if tiles[i, 1] == 0:
+            row0 = tiles[i, 3]
+            assert torch.equal(base[row0:row0 + wl.bl], step.out[row0:row0 + wl.bl])
+
+
+def test_packed_equals_each_request_alone():
+    """Sec. 4.2: packed execution equals per-request execution, bit for bit
+    (fixed split size so the key partitions are the same)."""
+    wl, host, t, step = setup("hetero64", seed=5, kv_split=512, B=6,
+                              layout="ragged")
+    log("[parity] packed vs alone")
+    step.run()
+    torch.cuda.synchronize()
+    g = gpu_results(step)
+    from paper_2607_17652_amd import synth
+    from paper_2607_17652_amd.runner import WavefrontStep
+    for b in range(wl.B):
+        wl1 = synth.workload("hetero64", B=1, layout="ragged")
+        h1 = {k: (v[b:b + 1].copy() if isinstance(v, np.ndarray) and v.ndim >= 1
+                  and v.shape[0] == wl.B else v) for k, v in host.items()}
+        h1["state"] = {k: v[b:b + 1].copy() for k, v in host["state"].items()}
+        rows = np.flatnonzero(g["row_req"] == b)
+        t1 = {k: t[k] for k in ("k_cache", "v_cache")}
+        cap1 = wl1.row_cap
+        for k in ("q", "k_new", "v_new", "logits"):
+            arr = torch.zeros((cap1,) + tuple(t[k].shape[1:]), dtype=t[k].dtype,
+                              device="cuda")
+            arr[:len(rows)] = t[k][torch.from_numpy(rows).cuda()]
+            t1[k] = arr
+        s1 = WavefrontStep(wl1, h1, t1, kv_split=512)
+        s1.run()
+        torch.cuda.synchronize()
+        assert torch.equal(s1.out[:len(rows)], step.out[torch.from_numpy(rows).cuda()])
+        assert torch.equal(s1.tokens[0], step.tokens[b])
+        assert torch.equal(s1.st[0], step.st[b])
+
+
+def test_all_inactive_is_a_noop():
+    def edit(wl, host):
+        host["state"]["active"][:] = 0
+    wl, host, t, step = setup("hetero64", seed=2, host_edit=edit)
+    log("[parity] all inactive")
+    before = step.tokens.clone()
+    st_before = step.st.clone()
+    step.run()
+    torch.cuda.synchronize()
+    s = fb.fb_pack_read_status(step.pack)
+    assert s["n_rows"] == 0 and s["n_tiles"] == 0 and s["code"] == 0
+    assert torch.equal(before, step.tokens)
+    assert torch.equal(st_before, step.st)
+
+
+def test_ill_formed_state_is_reported_and_skipped():
+    def edit(wl, host):
+        host["state"]["R"][3] = host["state"]["L"][3] + wl.W_max + 1
+    wl, host, t, step = setup("hetero64", seed=6, host_edit=edit)
+    log("[parity] ill-formed request 3")
+    st_before = step.st.clone()
+    step.run()
+    torch.cuda.synchronize()
+    s = fb.fb_pack_read_status(step.pack)
+    assert s["code"] == fb.FB_DERR_STATE and s["request"] == 3
+    assert torch.equal(st_before[3], step.st[3])
+    stats = fb.stats_to_numpy(step.stats, wl.B)
+    assert stats["valid"][3] == 0 and stats["valid"][2] == 1
+
+
+def test_bad_page_id_is_reported_without_fault():
+    def edit(wl, host):
+        host["page_table"][2, 1] = host["num_pages"] + 1000
+        host["page_table"][4, 0] = -5
+    wl, host, t, step = setup("hetero64", seed=6, host_edit=edit)
+    log("[parity] bad page ids in requests 2 and 4")
+    step.run()
+    torch.cuda.synchronize()
+    s = fb.fb_pack_read_status(step.pack)
+    assert s["code"] == fb.FB_DERR_PAGE and s["request"] == 2
+
+
+@pytest.mark.parametrize("flags", [dict(edit_masked=True),
+                                   dict(force_progress=True),
+                                   dict(eos=True)])
+def test_update_flags(flags):
+    flags = dict(flags)
+    eos = flags.pop("eos", False)
+    eos_id = 7
+
+    def edit(wl, host):
+        if eos:
+            # plant the EOS id in a fifth of the revealed window tokens so that
+            # retiring blocks hold it
+            rng = np.random.default_rng(0)
+            st = host["state"]
+            for b in range(wl.B):
+                o = int(host["o"][b])
+                for p in range(o, o + int(st["R"][b] - st["L"][b]) * wl.bl):
+                    if host["tokens"][b, p] != wl.mask_id and rng.uniform() < 0.2:
+                        host["tokens"][b, p] = eos_id
+    wl, host, t, step = setup("hetero64", seed=8, host_edit=edit,
+                              eos_id=eos_id if eos else -1)
+    log(f"[parity] flags {flags} eos={eos}")
+    p = dict(wl.params(), **flags)
+    step.set_params(flags=(fb.FB_EDIT_MASKED if p["edit_masked"] else 0) |
+                    (fb.FB_FORCE_PROGRESS if p["force_progress"] else 0))
+    case = OracleCase(wl, host, t, list(range(wl.B)), step.page_table)
+    step.run()
+    torch.cuda.synchronize()
+    g = gpu_results(step)
+    case.run(p, attention=False)
+    compare_case(wl, case, g, step, check_attention=False, check_kv=False)
+
+
+@pytest.mark.parametrize("name", ["tiny", "single", "hetero64"])
+def test_multi_step_matches_oracle(name):
+    """Four consecutive steps with fresh inputs each step: the GPU state and
+    the oracle state evolve identically (the oracle from its own results)."""
+    from oracle import attention as oatt, pack as opack, update as oupd
+    from paper_2607_17652_amd import synth
+    wl, host, t, step = setup(name, seed=9)
+    ost = {k: v.copy() for k, v in host["state"].items()}
+    otok, ope, ofin = host["tokens"].copy(), host["pe"].copy(), host["fin"].copy()
+    excluded = set()
+    for it in range(4):
+        log(f"[parity] multi-step {name} step {it}")
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(1000 + it)
+        t["logits"] = synth.make_logits(wl, wl.row_cap, gen, "cuda")
+        step.t = t
+        packed = opack.pack_wavefronts(ost, wl.W_max, wl.bl, wl.layout)
+        live = np.flatnonzero(packed["row_req"] >= 0)
+        xhat = np.full(packed["cap"], -1)
+        p64 = np.zeros(packed["cap"])
+        for c0 in range(0, len(live), 128):
+            r = live[c0:c0 + 128]
+            z = t["logits"][torch.from_numpy(r).cuda()].double().cpu().numpy()
+            xhat[r], p64[r] = oupd.vocab_reduce(z)
+        res = oupd.denoise_update(xhat, p64, otok, ost, ope, ofin, packed,
+                                  wl.params())
+        step.run()
+        torch.cuda.synchronize()
+        g = gpu_results(step)
+        assert np.array_equal(g["row_req"], packed["row_req"])
+        excluded |= set(res["band_reqs"])
+        for b in range(wl.B):
+            if b in excluded:
+                continue
+            assert np.array_equal(g["tokens"][b], res["tokens"][b]), (it, b)
+            for k in ("L", "R", "active"):
+                assert g["st"][k][b] == res["state"][k][b], (it, b, k)
+            assert np.array_equal(g["fin"][b], res["fin"][b]), (it, b)
+            assert np.array_equal(g["pe"][b], res["pe"][b]), (it, b)
+        ost, otok, ope, ofin = res["state"], res["tokens"], res["pe"], res["fin"]
+        if excluded:
+            log(f"[parity] band-excluded requests: {sorted(excluded)}")
