@@ -1,0 +1,308 @@
+#!/usr/bin/env python
+"""Benchmark of the packed wavefront denoising step on one MI355X.
+
+One step = pack (Eq. 4) + window KV write (Eq. 6) + block-causal attention
+(Sec. 4.1, one layer) + vocab reduction and denoise update (Eq. 1-3, Alg. 1)
+over one batch of a seeded synthetic workload whose inputs are resident in
+HBM before timing starts.  Every timed step starts from its own copy of the
+same request state, so all K steps do identical work.
+
+Prints ONE JSON line: active tokens/s (live window tokens, never padding),
+attention % of dense bf16 MFMA peak, update HBM GB/s, per-phase times from
+HIP events recorded on the launch stream, a roofline entry for the dominant
+kernel and the fp64 oracle timed on a bounded sample on the host cores.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload serve256]
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "active tokens/s per wavefront step; attn % MFMA peak; update HBM GB/s"
+PEAK_BF16_FLOPS = 2.5e15      # MI355X dense bf16 MFMA
+PEAK_HBM_BYTES = 8.0e12       # MI355X HBM3E
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="serve256")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def workload_work(wl, host):
+    """Live rows, attention flops over the visible keys, and algorithmic bytes."""
+    st = host["state"]
+    n_live = 0
+    flops = 0.0
+    kv_bytes = 0.0
+    elt = 2 if wl.dtype == "bf16" else 4
+    for b in range(wl.B):
+        if not st["active"][b]:
+            continue
+        w = int(st["R"][b] - st["L"][b])
+        o = int(st["gen_start"][b] + st["L"][b] * wl.bl)
+        n_live += w * wl.bl
+        for s in range(w):
+            flops += 4.0 * wl.bl * wl.Hq * wl.d * (o + (s + 1) * wl.bl)
+        if w:
+            kv_bytes += 2.0 * wl.Hkv * wl.d * elt * (o + w * wl.bl)
+    qo_bytes = 2.0 * n_live * wl.Hq * wl.d * elt
+    return n_live, flops, kv_bytes + qo_bytes
+
+
+def src_sha(name):
+    path = os.path.join(ROOT, "paper_2607_17652_amd", "csrc", name)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload, src_file):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            txt = f.read()
+        rec = json.loads(txt[txt.index("{"): txt.rindex("}") + 1])
+    except (ValueError, OSError):
+        return None
+    if rec.get("src_sha") != src_sha(src_file):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def copy_probe():
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "launches": 5}), flush=True)
+
+
+def gather_kv(k_cache, v_cache, pt_row, T, ps):
+    import torch
+    pos = torch.arange(T, device=k_cache.device)
+    pages = pt_row[pos // ps].long()
+    K = k_cache[pages, :, pos % ps, :]
+    V = v_cache[pages, :, :, pos % ps]
+    return K.double().cpu().numpy(), V.double().cpu().numpy()
+
+
+def cpu_baseline(wl, host, t, budget_s, seed):
+    """Time the fp64 oracle (as it stands) on whole requests, one at a time,
+    until the budget is spent; only the oracle's own computation is timed."""
+    import numpy as np
+    import torch
+    from oracle import attention as oatt
+    from oracle import pack as opack
+    from oracle import update as oupd
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    st = host["state"]
+    full = opack.pack_wavefronts(st, wl.W_max, wl.bl, wl.layout)
+    order = np.random.default_rng(seed + 99).permutation(wl.B)
+    spent, rows_done, reqs_done = 0.0, 0, 0
+    params = wl.params()
+    for b in order:
+        if not st["active"][b] or st["R"][b] == st["L"][b]:
+            continue
+        sub = {k: np.asarray(v)[[b]].copy() for k, v in st.items()}
+        sp = opack.pack_wavefronts(sub, wl.W_max, wl.bl, opack.RAGGED)
+        rf = np.flatnonzero(full["row_req"] == b)
+        rf = rf[np.argsort(full["row_pos"][rf])]
+        rs = np.flatnonzero(sp["row_req"] == 0)
+        rs = rs[np.argsort(sp["row_pos"][rs])]
+        idx = torch.from_numpy(rf).cuda()
+        cap = sp["cap"]
+        q = np.zeros((cap, wl.Hq, wl.d))
+        kn = np.zeros((cap, wl.Hkv, wl.d))
+        vn = np.zeros((cap, wl.Hkv, wl.d))
+        q[rs] = t["q"][idx].double().cpu().numpy()
+        kn[rs] = t["k_new"][idx].double().cpu().numpy()
+        vn[rs] = t["v_new"][idx].double().cpu().numpy()
+        z = np.zeros((cap, wl.V))
+        z[rs] = t["logits"][idx].double().cpu().numpy()
+        o = int(st["gen_start"][b] + st["L"][b] * wl.bl)
+        T = o + int(st["R"][b] - st["L"][b]) * wl.bl
+        K, V = gather_kv(t["k_cache"], t["v_cache"], torch.from_numpy(
+            host["page_table"][b]).cuda(), T, wl.page_size)
+        tok = host["tokens"][[b]].copy()
+        pe, fin = host["pe"][[b]].copy(), host["fin"][[b]].copy()
+        t0 = time.perf_counter()
+        p2 = opack.pack_wavefronts(sub, wl.W_max, wl.bl, opack.RAGGED)
+        K2, V2 = oatt.write_window_kv([K], [V], kn, vn, p2)
+        oatt.window_attention(q, K2, V2, p2, wl.Hq, wl.Hkv)
+        live = np.flatnonzero(p2["row_req"] >= 0)
+        xhat = np.full(cap, -1, dtype=np.int64)
+        p64 = np.zeros(cap)
+        xhat[live], p64[live] = oupd.vocab_reduce(z[live])
+        oupd.denoise_update(xhat, p64, tok, sub, pe, fin, p2, params)
+        spent += time.perf_counter() - t0
+        rows_done += len(live)
+        reqs_done += 1
+        if spent >= budget_s:
+            break
+    return {"value": rows_done / spent if spent > 0 else None, "unit": "tokens/s",
+            "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"{reqs_done} of {wl.B} requests ({rows_done} live tokens): "
+                      f"pack, KV write, attention, vocab reduction, update in fp64 "
+                      f"numpy; {spent:.1f} s; matmuls on {blas_threads} BLAS "
+                      f"threads, the rest on one"}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not "
+              f"supported (requests are independent, see the sharding notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
+    import numpy as np
+    import torch
+    from paper_2607_17652_amd import binding as fb
+    from paper_2607_17652_amd import synth
+    from paper_2607_17652_amd.runner import WavefrontStep
+
+    torch.cuda.set_device(0)
+    wl = synth.workload(args.workload)
+    host = synth.make_host_state(wl, args.seed)
+    t = synth.make_device_tensors(wl, host, args.seed, device="cuda")
+    step = WavefrontStep(wl, host, t)
+    n_live, flops, attn_bytes = workload_work(wl, host)
+    K, W = args.steps, args.warmup
+    copies = [(step.st.clone(), step.tokens.clone(), step.pe.clone(), step.fin.clone())
+              for _ in range(K + W)]
+    torch.cuda.synchronize()
+    print(f"[bench] workload={wl.name} B={wl.B} live_tokens={n_live} "
+          f"steps={K} warmup={W}", file=sys.stderr, flush=True)
+
+    nph = 5
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)]
+              for _ in range(K)]
+
+    def one_step(i, ev):
+        st, tok, pe, fin = copies[i]
+        if ev is not None:
+            ev[0].record()
+        fb.fb_pack_wavefronts(st, tok, step.n_max, step.T_max, step.pack)
+        if ev is not None:
+            ev[1].record()
+        fb.fb_write_window_kv(t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                              step.page_table, step.pack, step.shape)
+        if ev is not None:
+            ev[2].record()
+        fb.fb_wavefront_attention(t["q"], t["k_cache"], t["v_cache"],
+                                  step.page_table, step.pack, step.shape,
+                                  step.out, step.attn_ws)
+        if ev is not None:
+            ev[3].record()
+        fb.fb_vocab_reduce(t["logits"], step.pack, step.upd_ws)
+        if ev is not None:
+            ev[4].record()
+        fb.fb_denoise_apply(wl.V, tok, step.conf, step.argmax, st, pe, fin,
+                            step.pack, step.params, step.stats, step.upd_ws)
+        if ev is not None:
+            ev[5].record()
+
+    for i in range(W):
+        one_step(K + i, None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        one_step(i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    status = fb.fb_pack_read_status(step.pack)
+    if status["code"] != 0:
+        raise RuntimeError(f"device status {status}")
+    names = ["pack", "kv_write", "attention", "vocab_reduce", "update_apply"]
+    ph = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1])
+                            for i in range(K)])) for j, n in enumerate(names)}
+    ms_step = wall * 1e3 / K
+    t_attn = ph["attention"] * 1e-3
+    t_voc = ph["vocab_reduce"] * 1e-3
+    t_upd = (ph["vocab_reduce"] + ph["update_apply"]) * 1e-3
+    elt = 2 if wl.dtype == "bf16" else 4
+    nsplit = fb.fb_update_workspace_bytes(step.pack, wl.V) // (wl.row_cap * 16)
+    voc_bytes = n_live * wl.V * elt + n_live * nsplit * 16
+    upd_bytes = n_live * wl.V * elt + 16 * n_live
+    attn_frac = flops / t_attn / PEAK_BF16_FLOPS
+    voc_ach = voc_bytes / t_voc
+    voc_traffic = measured_traffic("vocab_pass", wl.name, "denoise.hip")
+    attn_traffic = measured_traffic("attn_bf16", wl.name, "attention.hip")
+    roof_voc = {"kernel": "vocab_pass_kernel", "bound": "hbm",
+                "achieved": voc_ach / 1e9, "peak": PEAK_HBM_BYTES / 1e9,
+                "unit": "GB/s", "frac": voc_ach / PEAK_HBM_BYTES,
+                "traffic": voc_traffic}
+    roof_attn = {"kernel": "fb_wavefront_attention (plan+attn_bf16+combine)",
+                 "bound": "mfma", "achieved": flops / t_attn / 1e12,
+                 "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
+                 "frac": attn_frac, "traffic": attn_traffic,
+                 "algorithmic_bytes": attn_bytes,
+                 "hbm_GBps_if_read_once": attn_bytes / t_attn / 1e9}
+    dominant, other = (roof_voc, roof_attn) if t_voc >= t_attn else (roof_attn, roof_voc)
+    out = {
+        "metric": METRIC,
+        "value": n_live / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv,
+                   "head_dim": wl.d, "bl": wl.bl, "W_max": wl.W_max,
+                   "layout": wl.layout, "page_size": wl.page_size, "V": wl.V,
+                   "live_tokens": n_live, "seed": args.seed},
+        "attn_pct_mfma_peak": 100.0 * attn_frac,
+        "update_hbm_gbps": upd_bytes / t_upd / 1e9,
+        "phases_ms": ph,
+        "roofline": dominant,
+        "roofline_other": other,
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
+        cb["host_cpus"] = os.cpu_count()
+        cb["cpu_model"] = cpu_model()
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

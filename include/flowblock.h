@@ -288,6 +288,25 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens,
                       fb_req_stats* stats, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* The two phases of fb_denoise_update, for callers that schedule or time
+ * them separately.  fb_denoise_update(...) is exactly fb_vocab_reduce
+ * followed by fb_denoise_apply on the same workspace.
+ *
+ * fb_vocab_reduce: step 1's streaming part (Eq. 1 symbols x_hat and p): for
+ * every live packed row, partial (max, lowest argmax, sum of exponentials)
+ * over vocabulary partitions, written to `ws`.  Reads each live logit once. */
+int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* fb_denoise_apply: steps 1 (merge of the partials: x_hat, p) through 5 of
+ * fb_denoise_update, from the workspace fb_vocab_reduce filled for the same
+ * pack and V. */
+int fb_denoise_apply(int V, int32_t* tokens, int T_max, float* conf,
+                     int32_t* argmax, fb_req_state* st, uint8_t* pe, uint8_t* fin,
+                     int n_max, const fb_pack* pack, const fb_update_params* prm,
+                     fb_req_stats* stats, const void* ws, size_t ws_bytes,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

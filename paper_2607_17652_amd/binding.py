@@ -39,6 +39,7 @@ EXPORTS = [
     "fb_pack_init", "fb_pack_wavefronts", "fb_pack_read_status",
     "fb_write_window_kv", "fb_attention_workspace_bytes",
     "fb_wavefront_attention", "fb_update_workspace_bytes", "fb_denoise_update",
+    "fb_vocab_reduce", "fb_denoise_apply",
 ]
 
 
@@ -118,6 +119,10 @@ def lib():
             "fb_denoise_update": (i32, [vp, i32, i32, vp, i32, vp, vp, vp, vp, vp,
                                         i32, P(fb_pack), P(fb_update_params), vp,
                                         vp, sz, vp]),
+            "fb_vocab_reduce": (i32, [vp, i32, i32, P(fb_pack), vp, sz, vp]),
+            "fb_denoise_apply": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, i32,
+                                       P(fb_pack), P(fb_update_params), vp, vp, sz,
+                                       vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -289,6 +294,21 @@ def fb_denoise_update(logits, tokens, conf, argmax, st, pe, fin, pack, params,
                                    _ptr(st), _ptr(pe), _ptr(fin), n_max,
                                    pack.ref(), ctypes.byref(params), _ptr(stats),
                                    _ptr(ws), nbytes, _stream(stream)))
+
+
+def fb_vocab_reduce(logits, pack, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib().fb_vocab_reduce(_ptr(logits), logits.shape[-1], _dtype_code(logits),
+                                 pack.ref(), _ptr(ws), nbytes, _stream(stream)))
+
+
+def fb_denoise_apply(V, tokens, conf, argmax, st, pe, fin, pack, params, stats, ws,
+                     stream=None):
+    nbytes = ws.numel() * ws.element_size()
+    _check(lib().fb_denoise_apply(V, _ptr(tokens), tokens.shape[-1], _ptr(conf),
+                                  _ptr(argmax), _ptr(st), _ptr(pe), _ptr(fin),
+                                  pe.shape[-1], pack.ref(), ctypes.byref(params),
+                                  _ptr(stats), _ptr(ws), nbytes, _stream(stream)))
 
 
 def stats_to_numpy(stats_tensor, B):

@@ -221,19 +221,14 @@ size_t fb_update_workspace_bytes(const fb_pack* pack, int V) {
     return fb::update_sizes(pack, V, cu_count()).total;
 }
 
-int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int T_max,
-                      float* conf, int32_t* argmax, fb_req_state* st, uint8_t* pe,
-                      uint8_t* fin, int n_max, const fb_pack* pack,
-                      const fb_update_params* prm, fb_req_stats* stats, void* ws,
-                      size_t ws_bytes, void* stream) {
-    int rc = check_pack(pack);
-    if (rc) return rc;
-    if (!logits || !tokens || !conf || !argmax || !st || !pe || !fin || !prm)
+namespace {
+
+int check_update_args(const fb_pack* pack, int V, const void* tokens, const void* conf,
+                      const void* argmax, const void* st, const void* pe, const void* fin,
+                      const fb_update_params* prm, int T_max, int n_max) {
+    if (!tokens || !conf || !argmax || !st || !pe || !fin || !prm)
         return fail(FB_E_INVAL, "a required pointer is NULL");
     if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
-    if (dtype != FB_BF16 && dtype != FB_F32)
-        return fail(FB_E_UNSUPPORTED, "logit dtype %d not supported", dtype);
-    if (!aligned16(logits)) return fail(FB_E_INVAL, "logits must be 16-byte aligned");
     if (T_max < 1 || n_max < 1) return fail(FB_E_INVAL, "T_max and n_max must be >= 1");
     if (prm->W < 1 || prm->W > pack->W_max)
         return fail(FB_E_INVAL, "W %d outside [1, W_max=%d]", prm->W, pack->W_max);
@@ -244,14 +239,80 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int
         return fail(FB_E_INVAL, "a threshold is NaN");
     if (prm->flags & ~(FB_EDIT_MASKED | FB_FORCE_PROGRESS))
         return fail(FB_E_INVAL, "unknown flag bits 0x%x", prm->flags);
-    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
-    if (ws_bytes < z.total || !ws)
+    return FB_OK;
+}
+
+int check_reduce_args(const fb_pack* pack, const void* logits, int V, int dtype) {
+    if (!logits) return fail(FB_E_INVAL, "logits is NULL");
+    if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
+    if (dtype != FB_BF16 && dtype != FB_F32)
+        return fail(FB_E_UNSUPPORTED, "logit dtype %d not supported", dtype);
+    if (!aligned16(logits)) return fail(FB_E_INVAL, "logits must be 16-byte aligned");
+    (void)pack;
+    return FB_OK;
+}
+
+int check_ws(const void* ws, size_t ws_bytes, size_t need) {
+    if (ws_bytes < need || !ws)
         return fail(FB_E_WORKSPACE, "update workspace has %zu bytes, needs %zu", ws_bytes,
-                    z.total);
+                    need);
     if (!aligned16(ws)) return fail(FB_E_INVAL, "workspace must be 16-byte aligned");
-    hipError_t e = fb::launch_update(logits, V, dtype, tokens, T_max, conf, argmax, st, pe,
-                                     fin, n_max, pack, prm, stats, ws, z,
-                                     (hipStream_t)stream);
+    return FB_OK;
+}
+
+}  // namespace
+
+int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack, void* ws,
+                    size_t ws_bytes, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_reduce_args(pack, logits, V, dtype);
+    if (rc) return rc;
+    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
+    rc = check_ws(ws, ws_bytes, z.total);
+    if (rc) return rc;
+    hipError_t e = fb::launch_vocab_reduce(logits, V, dtype, pack, ws, z,
+                                           (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "vocab reduction launch");
+    return ok();
+}
+
+int fb_denoise_apply(int V, int32_t* tokens, int T_max, float* conf, int32_t* argmax,
+                     fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
+                     const fb_pack* pack, const fb_update_params* prm,
+                     fb_req_stats* stats, const void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_update_args(pack, V, tokens, conf, argmax, st, pe, fin, prm, T_max, n_max);
+    if (rc) return rc;
+    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
+    rc = check_ws(ws, ws_bytes, z.total);
+    if (rc) return rc;
+    hipError_t e = fb::launch_apply(tokens, T_max, conf, argmax, st, pe, fin, n_max, pack,
+                                    prm, stats, ws, z, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "update launch");
+    return ok();
+}
+
+int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int T_max,
+                      float* conf, int32_t* argmax, fb_req_state* st, uint8_t* pe,
+                      uint8_t* fin, int n_max, const fb_pack* pack,
+                      const fb_update_params* prm, fb_req_stats* stats, void* ws,
+                      size_t ws_bytes, void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_reduce_args(pack, logits, V, dtype);
+    if (rc) return rc;
+    rc = check_update_args(pack, V, tokens, conf, argmax, st, pe, fin, prm, T_max, n_max);
+    if (rc) return rc;
+    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
+    rc = check_ws(ws, ws_bytes, z.total);
+    if (rc) return rc;
+    hipError_t e = fb::launch_vocab_reduce(logits, V, dtype, pack, ws, z,
+                                           (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "vocab reduction launch");
+    e = fb::launch_apply(tokens, T_max, conf, argmax, st, pe, fin, n_max, pack, prm, stats,
+                         ws, z, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "update launch");
     return ok();
 }

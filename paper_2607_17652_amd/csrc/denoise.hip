@@ -398,12 +398,9 @@ UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count) {
     return z;
 }
 
-hipError_t launch_update(const void* logits, int V, int dtype, int32_t* tokens,
-                         int T_max, float* conf, int32_t* argmax,
-                         fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
-                         const fb_pack* pack, const fb_update_params* p,
-                         fb_req_stats* stats, void* ws, const UpdateSizes& z,
-                         hipStream_t stream) {
+hipError_t launch_vocab_reduce(const void* logits, int V, int dtype,
+                               const fb_pack* pack, void* ws, const UpdateSizes& z,
+                               hipStream_t stream) {
     PackView pv = pack_view(pack);
     float4* part = static_cast<float4*>(ws);
     const dim3 grid((unsigned)pack->row_cap * (unsigned)z.nsplit);
@@ -416,15 +413,23 @@ hipError_t launch_update(const void* logits, int V, int dtype, int32_t* tokens,
                            stream, static_cast<const float*>(logits), V, z.nsplit,
                            z.chunk, pv, part);
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    return hipGetLastError();
+}
+
+hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax,
+                        fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
+                        const fb_pack* pack, const fb_update_params* p,
+                        fb_req_stats* stats, const void* ws, const UpdateSizes& z,
+                        hipStream_t stream) {
+    PackView pv = pack_view(pack);
     UpdParams prm{p->tau_mask, p->tau_edit, p->theta_spawn, p->mask_id,
                   p->eos_id,   p->S_pe,     p->W,           p->flags};
     const size_t rows_cap = (size_t)pack->W_max * pack->bl;
     const size_t smem = rows_cap * (sizeof(float) + sizeof(int) + 1);
     hipLaunchKernelGGL(request_kernel, dim3(pack->B), dim3(kUpdThreads), smem, stream,
-                       part, z.nsplit, pv, tokens, T_max, conf, argmax, st, pe, fin,
-                       n_max, pack->bl, pack->W_max, prm, stats);
+                       static_cast<const float4*>(ws), z.nsplit, pv, tokens, T_max,
+                       conf, argmax, st, pe, fin, n_max, pack->bl, pack->W_max, prm,
+                       stats);
     return hipGetLastError();
 }
 

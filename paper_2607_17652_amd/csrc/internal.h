@@ -82,11 +82,13 @@ struct UpdateSizes {
     size_t total;    // workspace bytes
 };
 UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count);
-hipError_t launch_update(const void* logits, int V, int dtype, int32_t* tokens,
-                         int T_max, float* conf, int32_t* argmax,
-                         fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
-                         const fb_pack* pack, const fb_update_params* prm,
-                         fb_req_stats* stats, void* ws, const UpdateSizes& sz,
-                         hipStream_t stream);
+hipError_t launch_vocab_reduce(const void* logits, int V, int dtype,
+                               const fb_pack* pack, void* ws, const UpdateSizes& sz,
+                               hipStream_t stream);
+hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax,
+                        fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
+                        const fb_pack* pack, const fb_update_params* prm,
+                        fb_req_stats* stats, const void* ws, const UpdateSizes& sz,
+                        hipStream_t stream);
 
 }  // namespace fb
