@@ -32,6 +32,7 @@ constexpr int kRowsPerWg = 128;     // 4 waves x 32 query rows
 constexpr int kAttnThreads = 256;
 constexpr int kKeyTile = 32;
 constexpr int kMinChunkTiles = 4;   // never split below 128 keys
+constexpr int kMaxSplits = 64;      // splits of one unit the combine can merge
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;  // lazy rescale: running max may lag by 2^8
 
@@ -117,18 +118,21 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         chunk = (total_tiles + target_items - 1) / target_items;
         if (chunk < kMinChunkTiles) chunk = kMinChunkTiles;
     }
-    // Grow the split size until the items and partial slots fit.
+    // Grow the split size until the items and partial slots fit and no unit
+    // has more splits than the combine merges.
     for (;;) {
-        long long my_items = 0, my_slots = 0;
+        long long my_items = 0, my_slots = 0, my_over = 0;
         for (int u = threadIdx.x; u < n_units; u += kPlanThreads) {
             const long long kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
             const long long ns = (kt + chunk - 1) / chunk;
             my_items += ns;
             if (ns > 1) my_slots += ns;
+            if (ns > kMaxSplits) my_over += 1;
         }
         const long long items = wg_sum_ll(my_items, sum_lds);
         const long long slots = wg_sum_ll(my_slots, sum_lds);
-        if (items <= item_cap && slots <= slot_cap) break;
+        const long long over = wg_sum_ll(my_over, sum_lds);
+        if (items <= item_cap && slots <= slot_cap && over == 0) break;
         chunk *= 2;
     }
 
@@ -188,26 +192,63 @@ __device__ inline float wave_xor32_max(float x) {
     return fmaxf(x, __shfl_xor(x, 32, 64));
 }
 
-template <int D>
-struct __attribute__((aligned(16))) Bf16Tiles {
-    static constexpr int kRowK = D + 8;            // K tile row, padded
-    static constexpr int kRowV = kKeyTile + 8;     // V^T tile row, padded
-    uint16_t k[2][kKeyTile * kRowK];
-    uint16_t v[2][D * kRowV];
-};
+// K/V staging: a ring of kStages key tiles in LDS, filled by direct
+// global->LDS loads (global_load_lds_dwordx4: lane i of a wave writes 16 bytes
+// at M0 + 16*i).  A stage holds the K tile [32 keys][D] followed by the V^T
+// tile [D][32 keys], both in 16-byte chunks whose position inside a row is
+// XOR-swizzled (K: chunk ^ (key % (D/8)); V^T: chunk ^ ((d/4) % 4)) so that
+// the MFMA operand reads of 16 lanes hit 16 distinct bank groups.  The loads
+// are issued from inline asm so the compiler neither sees nor waits on them;
+// the kernel orders them itself with explicit vmcnt waits and raw barriers.
+constexpr int kStages = 4;
 
 template <int D>
-__global__ void __launch_bounds__(kAttnThreads)
+struct Ring {
+    static constexpr int kKCh = kKeyTile * D / 8;   // K chunks per stage
+    static constexpr int kVCh = D * kKeyTile / 8;   // V^T chunks per stage
+    static constexpr int kCh = kKCh + kVCh;
+    static constexpr int kStageBytes = kCh * 16;
+    static constexpr int kPerThread = kCh / kAttnThreads;   // D / 32
+    static_assert(kCh % kAttnThreads == 0, "chunks must divide the workgroup");
+};
+
+__device__ inline void dma16(const void* src, uint32_t lds_wave_base) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(lds_wave_base), "v"(src) : "memory");
+}
+
+__device__ inline void barrier_raw() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Wait until at most n of this wave's vector-memory loads are outstanding.
+__device__ inline void wait_vm(int n) {
+    switch (n) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+}
+
+template <int D>
+__global__ void __launch_bounds__(kAttnThreads, 2)
 attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                  const uint16_t* __restrict__ v_cache,
                  const int32_t* __restrict__ page_table, PackView pv, AttnWs ws,
                  uint16_t* __restrict__ out, int Hq, int Hkv, int g, int bl, int RG,
                  int ps, int ps_shift, int max_pages, int num_pages, float scale_log2) {
-    __shared__ Bf16Tiles<D> sm;
+    using RG_ = Ring<D>;
+    __shared__ __attribute__((aligned(16))) unsigned char ring[kStages * RG_::kStageBytes];
     constexpr int KK = D / 16;      // k-steps of the S^T product
     constexpr int DT = D / 32;      // 32-wide d tiles of O^T
-    constexpr int NCH = D / 32;     // 16-byte loads per thread per key tile
-    constexpr int KCH = 4 * D;      // K chunks per tile (32 keys x D/8)
+    constexpr int NCH = RG_::kPerThread;
+    constexpr int CPR = D / 8;      // 16-byte chunks per K row
 
     const int item = blockIdx.x;
     if (item >= ws.counts[kCItems]) return;
@@ -221,8 +262,9 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const int row0 = tile[kTRow0];
     const int32_t* pt = page_table + (size_t)b * max_pages;
 
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
     const int n = lane & 31;
     const int h = lane >> 5;
     const int r_local = wave * 32 + n;
@@ -232,15 +274,69 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const int hg = row_ok ? r % g : 0;
     const size_t q_off = ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D;
 
+    // Q fragments go to registers first; the asm barrier makes the compiler
+    // finish these loads before any ring load is issued.
     bf16x8 qf[KK];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-        if (row_ok) {
-            qf[kk] = *reinterpret_cast<const bf16x8*>(q + q_off + kk * 16 + h * 8);
+        if (row_ok) qf[kk] = *reinterpret_cast<const bf16x8*>(q + q_off + kk * 16 + h * 8);
+        else qf[kk] = bf16x8{};
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) asm volatile("" :: "v"(qf[kk]));
+
+    // Per-thread chunk geometry (the same for every key tile).
+    int ch_key[NCH];      // key offset in the tile of the chunk's first key
+    int ch_off[NCH];      // element offset inside a page (without the slot term)
+    bool ch_isk[NCH];
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const int s = j * kAttnThreads + tid;
+        if (s < RG_::kKCh) {
+            const int key = s / CPR;
+            const int dchunk = (s % CPR) ^ (key % CPR);
+            ch_isk[j] = true;
+            ch_key[j] = key;
+            ch_off[j] = dchunk * 8;
         } else {
-            qf[kk] = bf16x8{};
+            const int s2 = s - RG_::kKCh;
+            const int d = s2 >> 2;
+            const int kc = (s2 & 3) ^ ((d >> 2) & 3);
+            ch_isk[j] = false;
+            ch_key[j] = kc * 8;
+            ch_off[j] = d * ps;
         }
     }
+    const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0];
+
+    auto issue_tile = [&](int kt, int stage) {
+        const int key0 = kt * kKeyTile;
+        const int pbase = key0 >> ps_shift;
+        const int plast = (ke - 1) >> ps_shift;   // last page below ke
+        // page ids are uniform across the workgroup: scalar loads
+        int pid[4];
+        const int npg = ps >= kKeyTile ? 1 : kKeyTile / ps;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pid[i] = (i < npg && pbase + i <= plast) ? pt[pbase + i] : -1;
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            const int kg = key0 + ch_key[j];
+            const int pi = (kg >> ps_shift) - pbase;
+            int page = pid[0];
+#pragma unroll
+            for (int i = 1; i < 4; ++i) page = pi == i ? pid[i] : page;
+            const bool ok = kg < ke && page >= 0 && page < num_pages;
+            if (kg < ke && !ok) record_error(pv.hdr, b, FB_DERR_PAGE);
+            const uint16_t* src = k_cache;
+            if (ok) {
+                const size_t ph = (size_t)page * Hkv + c;
+                src = ch_isk[j] ? k_cache + (ph * ps + (kg & (ps - 1))) * D + ch_off[j]
+                                : v_cache + ph * D * ps + ch_off[j] + (kg & (ps - 1));
+            }
+            dma16(src, __builtin_amdgcn_readfirstlane(
+                ring_base + stage * RG_::kStageBytes + j * 4096 + wave * 1024));
+        }
+    };
 
     floatx16 o[DT];
 #pragma unroll
@@ -249,97 +345,56 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     float l_part = 0.f;        // this lane's share of the softmax denominator
 
     const int kt0 = kb / kKeyTile;
-    const int kt1 = (ke + kKeyTile - 1) / kKeyTile;
-
-    uint4 stage[NCH];
-    auto load_tile = [&](int kt) {
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-            const int e = threadIdx.x + j * kAttnThreads;
-            uint4 val = make_uint4(0, 0, 0, 0);
-            if (e < KCH) {
-                const int key = e / (D / 8);
-                const int dc = e % (D / 8);
-                const int kg = kt * kKeyTile + key;
-                if (kg < ke) {
-                    const int page = pt[kg >> ps_shift];
-                    if (page >= 0 && page < num_pages) {
-                        const size_t off = (((size_t)page * Hkv + c) * ps + (kg & (ps - 1))) * D + dc * 8;
-                        val = *reinterpret_cast<const uint4*>(k_cache + off);
-                    } else if (dc == 0) {
-                        record_error(pv.hdr, b, FB_DERR_PAGE);
-                    }
-                }
-            } else {
-                const int e2 = e - KCH;
-                const int d = e2 >> 2;
-                const int kc = e2 & 3;
-                const int kg = kt * kKeyTile + kc * 8;
-                const int nvalid = ke - kg;
-                const int page = nvalid > 0 ? pt[kg >> ps_shift] : -1;
-                if (nvalid > 0 && page >= 0 && page < num_pages) {
-                    const size_t off = (((size_t)page * Hkv + c) * D + d) * ps + (kg & (ps - 1));
-                    val = *reinterpret_cast<const uint4*>(v_cache + off);
-                    if (nvalid < 8) {
-                        uint32_t w[4] = {val.x, val.y, val.z, val.w};
-#pragma unroll
-                        for (int x = 0; x < 8; ++x) {
-                            if (x >= nvalid) w[x >> 1] &= (x & 1) ? 0x0000ffffu : 0xffff0000u;
-                        }
-                        val = make_uint4(w[0], w[1], w[2], w[3]);
-                    }
-                }
-            }
-            stage[j] = val;
-        }
-    };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-            const int e = threadIdx.x + j * kAttnThreads;
-            if (e < KCH) {
-                const int key = e / (D / 8);
-                const int dc = e % (D / 8);
-                *reinterpret_cast<uint4*>(&sm.k[buf][key * Bf16Tiles<D>::kRowK + dc * 8]) = stage[j];
-            } else {
-                const int e2 = e - KCH;
-                const int d = e2 >> 2;
-                const int kc = e2 & 3;
-                *reinterpret_cast<uint4*>(&sm.v[buf][d * Bf16Tiles<D>::kRowV + kc * 8]) = stage[j];
-            }
-        }
-    };
-
+    const int nt = (ke + kKeyTile - 1) / kKeyTile - kt0;
     const int krow = swap_bits23(n);
-    if (kt0 < kt1) {
-        load_tile(kt0);
-        store_tile(0);
-    }
-    __syncthreads();
-    for (int kt = kt0; kt < kt1; ++kt) {
-        const int buf = (kt - kt0) & 1;
-        const bool more = kt + 1 < kt1;
-        if (more) load_tile(kt + 1);
+    const int kswz = krow % CPR;
+
+#pragma unroll
+    for (int p = 0; p < kStages - 1; ++p)
+        if (p < nt) issue_tile(kt0 + p, p);
+
+    for (int i = 0; i < nt; ++i) {
+        const int kt = kt0 + i;
+        const int stage = i % kStages;
+        const int later = min(kStages - 2, nt - 1 - i);
+        wait_vm(later * NCH);
+        barrier_raw();
+        if (i + kStages - 1 < nt) issue_tile(kt + kStages - 1, (i + kStages - 1) % kStages);
+        const unsigned char* sbase = ring + stage * RG_::kStageBytes;
+        const uint16_t* klds = reinterpret_cast<const uint16_t*>(sbase);
+        uint16_t* vlds = reinterpret_cast<uint16_t*>(const_cast<unsigned char*>(sbase) +
+                                                     RG_::kKCh * 16);
+        const int valid = ke - kt * kKeyTile;      // keys of this tile below ke
+        if (valid < kKeyTile) {
+            // Zero V^T for the keys past ke so 0-weight products stay 0.
+            for (int e = tid; e < D * kKeyTile; e += kAttnThreads) {
+                const int d = e / kKeyTile, key = e % kKeyTile;
+                if (key >= valid) {
+                    const int pos = (key >> 3) ^ ((d >> 2) & 3);
+                    vlds[d * kKeyTile + pos * 8 + (key & 7)] = 0;
+                }
+            }
+            barrier_raw();
+        }
 
         // S^T (32 keys x 32 rows) = K Q^T
         floatx16 s = floatx16{};
-        const uint16_t* kbase = &sm.k[buf][krow * Bf16Tiles<D>::kRowK + h * 8];
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbase + kk * 16);
+            const int chunk = (kk * 2 + h) ^ kswz;
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(klds + krow * D + chunk * 8);
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
         }
-        // Mask keys at or past ke (only the last tile can have any).
-        if (kt * kKeyTile + kKeyTile > ke) {
+        if (valid < kKeyTile) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int key = 16 * (i >> 3) + 8 * h + (i & 7);
-                if (kt * kKeyTile + key >= ke) s[i] = -INFINITY;
+            for (int x = 0; x < 16; ++x) {
+                const int key = 16 * (x >> 3) + 8 * h + (x & 7);
+                if (key >= valid) s[x] = -INFINITY;
             }
         }
         float mx = s[0];
 #pragma unroll
-        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s[i]);
+        for (int x = 1; x < 16; ++x) mx = fmaxf(mx, s[x]);
         mx = wave_xor32_max(mx) * scale_log2;
         const bool need = mx > m_run + kRescaleSlack;
         if (__any(need)) {
@@ -348,29 +403,29 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
+                for (int x = 0; x < 16; ++x) o[dt][x] *= alpha;
             l_part *= alpha;
             m_run = m_new;
         }
         bf16x8 pb[2];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[i], scale_log2, -m_run));
+        for (int x = 0; x < 16; ++x) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[x], scale_log2, -m_run));
             l_part += p;
-            pb[i >> 3][i & 7] = (__bf16)p;
+            pb[x >> 3][x & 7] = (__bf16)p;
         }
         // O^T (d x 32 rows) += V^T (d x 32 keys) P^T (32 keys x 32 rows)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            const uint16_t* vbase = &sm.v[buf][(dt * 32 + n) * Bf16Tiles<D>::kRowV + h * 8];
+            const int d = dt * 32 + n;
+            const int vsw = (d >> 2) & 3;
 #pragma unroll
             for (int tt = 0; tt < 2; ++tt) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(vbase + tt * 16);
+                const int pos = (tt * 2 + h) ^ vsw;
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(vlds + d * kKeyTile + pos * 8);
                 o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[tt], o[dt], 0, 0, 0);
             }
         }
-        if (more) store_tile(buf ^ 1);
-        __syncthreads();
     }
 
     const float l = l_part + __shfl_xor(l_part, 32, 64);
@@ -416,10 +471,17 @@ __device__ inline void store_out<uint16_t>(uint16_t* p, float v) {
 template <>
 __device__ inline void store_out<float>(float* p, float v) { *p = v; }
 
+// One workgroup per split unit: the per-split log-sum-exp weights of each
+// row are computed once into LDS, then every thread merges 4 consecutive d
+// of a row with 16-byte loads.
+constexpr int kMaxSplitsLds = kMaxSplits;
+
 template <typename T>
 __global__ void __launch_bounds__(kAttnThreads)
 combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
                int g, int bl, int RG, int D) {
+    __shared__ float wgt[kMaxSplitsLds][kRowsPerWg];
+    __shared__ float inv_den[kRowsPerWg];
     const int u = blockIdx.x;
     if (u >= ws.counts[kCUnits]) return;
     const int ns = ws.units[(size_t)u * 2 + kUSplits];
@@ -429,23 +491,44 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
     const int c = (u / RG) % Hkv;
     const int t = u / (RG * Hkv);
     const int row0 = pv.tiles[(size_t)t * kTileInts + kTRow0];
-    for (int e = threadIdx.x; e < kRowsPerWg * D; e += kAttnThreads) {
-        const int rl = e / D;
-        const int d = e % D;
-        const int r = rg * kRowsPerWg + rl;
-        if (r >= bl * g) break;
+    const int nrows = min(kRowsPerWg, bl * g - rg * kRowsPerWg);
+    const int nsl = min(ns, kMaxSplitsLds);
+    for (int rl = threadIdx.x; rl < nrows; rl += kAttnThreads) {
         float mx = -INFINITY;
         for (int k = 0; k < ns; ++k)
             mx = fmaxf(mx, ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl]);
-        float num = 0.f, den = 0.f;
+        float den = 0.f;
         for (int k = 0; k < ns; ++k) {
-            const float wgt = __builtin_amdgcn_exp2f(
+            const float w = __builtin_amdgcn_exp2f(
                 ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl] - mx);
-            num += wgt * ws.part_o[((size_t)(slot0 + k) * kRowsPerWg + rl) * D + d];
-            den += wgt;
+            if (k < nsl) wgt[k][rl] = w;
+            den += w;
         }
+        inv_den[rl] = 1.0f / den;
+    }
+    __syncthreads();
+    const int per_row = D / 4;
+    for (int e = threadIdx.x; e < nrows * per_row; e += kAttnThreads) {
+        const int rl = e / per_row;
+        const int d0 = (e % per_row) * 4;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int k = 0; k < nsl; ++k) {
+            const float w = wgt[k][rl];
+            const float4 v = *reinterpret_cast<const float4*>(
+                ws.part_o + ((size_t)(slot0 + k) * kRowsPerWg + rl) * D + d0);
+            acc.x += w * v.x;
+            acc.y += w * v.y;
+            acc.z += w * v.z;
+            acc.w += w * v.w;
+        }
+        const float id = inv_den[rl];
+        const int r = rg * kRowsPerWg + rl;
         const int pos_local = r / g, hg = r % g;
-        store_out<T>(out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d, num / den);
+        T* dst = out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d0;
+        store_out<T>(dst + 0, acc.x * id);
+        store_out<T>(dst + 1, acc.y * id);
+        store_out<T>(dst + 2, acc.z * id);
+        store_out<T>(dst + 3, acc.w * id);
     }
 }
 
