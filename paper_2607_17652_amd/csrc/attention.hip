@@ -20,6 +20,8 @@
 //                  in the exp2 domain with lazy rescaling
 //   combine        merges split partials with their log-sum-exp weights
 //   attn_f32       a plain fp32 path (small problems, exactness reference)
+#include <type_traits>
+
 #include "internal.h"
 
 namespace fb {
@@ -274,7 +276,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const int hg = row_ok ? r % g : 0;
     const size_t q_off = ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D;
 
-    // Q fragments go to registers first; the asm barrier makes the compiler
+    // Q fragments go to registers first; the empty asm makes the compiler
     // finish these loads before any ring load is issued.
     bf16x8 qf[KK];
 #pragma unroll
@@ -285,9 +287,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) asm volatile("" :: "v"(qf[kk]));
 
-    // Per-thread chunk geometry (the same for every key tile).
-    int ch_key[NCH];      // key offset in the tile of the chunk's first key
-    int ch_off[NCH];      // element offset inside a page (without the slot term)
+    // Per-thread chunk geometry, the same for every key tile: byte offset of
+    // the chunk inside its page (K: [slot][d], V^T: [d][slot]) and the key
+    // offset of its first key inside the tile.  Each (load j, wave) is all-K
+    // or all-V, so the global base can be a wave-uniform scalar pair.
+    uint32_t ch_off[NCH];
+    int ch_key[NCH];
     bool ch_isk[NCH];
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
@@ -297,44 +302,99 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             const int dchunk = (s % CPR) ^ (key % CPR);
             ch_isk[j] = true;
             ch_key[j] = key;
-            ch_off[j] = dchunk * 8;
+            ch_off[j] = (uint32_t)(key * D + dchunk * 8) * 2u;
         } else {
             const int s2 = s - RG_::kKCh;
             const int d = s2 >> 2;
             const int kc = (s2 & 3) ^ ((d >> 2) & 3);
             ch_isk[j] = false;
             ch_key[j] = kc * 8;
-            ch_off[j] = d * ps;
+            ch_off[j] = (uint32_t)(d * ps + kc * 8) * 2u;
         }
     }
+    uint32_t m0_base[NCH];
     const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0];
+#pragma unroll
+    for (int j = 0; j < NCH; ++j)
+        m0_base[j] = __builtin_amdgcn_readfirstlane(ring_base + j * 4096 + wave * 1024);
+    const size_t k_head = (size_t)c * ps * D;        // head c inside a K page
+    const size_t v_head = (size_t)c * D * ps;        // head c inside a V page
+    const size_t page_elems = (size_t)Hkv * ps * D;  // one page of one cache
 
-    auto issue_tile = [&](int kt, int stage) {
+    // Per-lane LDS byte offsets of the MFMA operand reads (stage 0).
+    const int krow = swap_bits23(n);
+    const int kswz = krow % CPR;
+    uint32_t koff[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+        koff[kk] = (uint32_t)(krow * D + (((kk * 2 + h) ^ kswz) * 8)) * 2u;
+    uint32_t voff[DT][2];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int d = dt * 32 + n;
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+            voff[dt][tt] = RG_::kKCh * 16 +
+                           (uint32_t)(d * kKeyTile + (((tt * 2 + h) ^ ((d >> 2) & 3)) * 8)) * 2u;
+    }
+
+    // Issue the loads of key tile kt into stage STAGE.
+    auto issue_tile = [&](int kt, auto stage_c) {
+        constexpr int STAGE = decltype(stage_c)::value;
         const int key0 = kt * kKeyTile;
-        const int pbase = key0 >> ps_shift;
-        const int plast = (ke - 1) >> ps_shift;   // last page below ke
-        // page ids are uniform across the workgroup: scalar loads
-        int pid[4];
-        const int npg = ps >= kKeyTile ? 1 : kKeyTile / ps;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pid[i] = (i < npg && pbase + i <= plast) ? pt[pbase + i] : -1;
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-            const int kg = key0 + ch_key[j];
-            const int pi = (kg >> ps_shift) - pbase;
-            int page = pid[0];
-#pragma unroll
-            for (int i = 1; i < 4; ++i) page = pi == i ? pid[i] : page;
-            const bool ok = kg < ke && page >= 0 && page < num_pages;
-            if (kg < ke && !ok) record_error(pv.hdr, b, FB_DERR_PAGE);
-            const uint16_t* src = k_cache;
-            if (ok) {
-                const size_t ph = (size_t)page * Hkv + c;
-                src = ch_isk[j] ? k_cache + (ph * ps + (kg & (ps - 1))) * D + ch_off[j]
-                                : v_cache + ph * D * ps + ch_off[j] + (kg & (ps - 1));
+        if (ps >= kKeyTile) {
+            // one page per tile: uniform base + per-lane constant offsets
+            int page = pt[key0 >> ps_shift];
+            if (page < 0 || page >= num_pages) {
+                record_error(pv.hdr, b, FB_DERR_PAGE);
+                page = 0;
             }
-            dma16(src, __builtin_amdgcn_readfirstlane(
-                ring_base + stage * RG_::kStageBytes + j * 4096 + wave * 1024));
+            const size_t inpage = (size_t)(key0 & (ps - 1));
+            const uint16_t* kbase = k_cache + (size_t)page * page_elems + k_head + inpage * D;
+            const uint16_t* vbase = v_cache + (size_t)page * page_elems + v_head + inpage;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+                const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
+                if (ch_isk[j])
+                    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                                 :: "s"(m0), "v"(ch_off[j]), "s"(kbase) : "memory");
+                else
+                    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                                 :: "s"(m0), "v"(ch_off[j]), "s"(vbase) : "memory");
+            }
+        } else {
+            // several pages per tile: per-lane page selection
+            const int pbase = key0 >> ps_shift;
+            const int plast = (ke - 1) >> ps_shift;
+            int pid[4];
+            const int npg = kKeyTile / ps;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                pid[i] = (i < npg && pbase + i <= plast) ? pt[pbase + i] : -1;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+                const int kg = key0 + ch_key[j];
+                const int pi = (kg >> ps_shift) - pbase;
+                int page = pid[0];
+#pragma unroll
+                for (int i = 1; i < 4; ++i) page = pi == i ? pid[i] : page;
+                const bool ok = kg < ke && page >= 0 && page < num_pages;
+                if (kg < ke && !ok) record_error(pv.hdr, b, FB_DERR_PAGE);
+                const unsigned char* src = reinterpret_cast<const unsigned char*>(k_cache);
+                if (ok) {
+                    const size_t inpage = (size_t)(kg & (ps - 1)) - (size_t)ch_key[j] % ps;
+                    const uint16_t* base =
+                        ch_isk[j] ? k_cache + (size_t)page * page_elems + k_head + (size_t)(kg & (ps - 1)) * D -
+                                        (size_t)ch_key[j] * D
+                                  : v_cache + (size_t)page * page_elems + v_head + (kg & (ps - 1)) -
+                                        ch_key[j];
+                    (void)inpage;
+                    src = reinterpret_cast<const unsigned char*>(base) + ch_off[j];
+                }
+                const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
+                asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                             :: "s"(m0), "v"(src) : "memory");
+            }
         }
     };
 
@@ -342,31 +402,39 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = floatx16{};
     float m_run = -INFINITY;   // running max of scores, log2 domain
-    float l_part = 0.f;        // this lane's share of the softmax denominator
+    float l_acc[2] = {0.f, 0.f};   // this lane's share of the denominator
+    bf16x8 pb[2];              // P^T of the previous tile, waiting for its PV
+    const bf16x8 ones = {(__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f,
+                         (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f};
 
     const int kt0 = kb / kKeyTile;
     const int nt = (ke + kKeyTile - 1) / kKeyTile - kt0;
-    const int krow = swap_bits23(n);
-    const int kswz = krow % CPR;
 
-#pragma unroll
-    for (int p = 0; p < kStages - 1; ++p)
-        if (p < nt) issue_tile(kt0 + p, p);
+    auto pv_mfma = [&](const unsigned char* vst, int dt, int tt) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vst + voff[dt][tt]);
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[tt], o[dt], 0, 0, 0);
+    };
 
-    for (int i = 0; i < nt; ++i) {
+    // One key tile i: wait for its stage; refill the stage of tile i-2 (free
+    // once every wave has passed this barrier: its PV ran in step i-1) with
+    // tile i+2; then S^T = K Q^T interleaved with the pending O^T += V^T P^T
+    // of tile i-1 (whose stage stays untouched until step i+1); then the
+    // online softmax of tile i.  Stages in use: i-1, i, i+1, i+2.
+    static_assert(kStages == 4, "the refill distance assumes four stages");
+    auto step = [&](int i, auto stage_c) {
+        constexpr int STAGE = decltype(stage_c)::value;
+        constexpr int NEXT = (STAGE + 2) % kStages;
         const int kt = kt0 + i;
-        const int stage = i % kStages;
-        const int later = min(kStages - 2, nt - 1 - i);
-        wait_vm(later * NCH);
+        if (i + 1 < nt) wait_vm(NCH);    // tile i+1 may still be in flight
+        else wait_vm(0);
         barrier_raw();
-        if (i + kStages - 1 < nt) issue_tile(kt + kStages - 1, (i + kStages - 1) % kStages);
-        const unsigned char* sbase = ring + stage * RG_::kStageBytes;
-        const uint16_t* klds = reinterpret_cast<const uint16_t*>(sbase);
-        uint16_t* vlds = reinterpret_cast<uint16_t*>(const_cast<unsigned char*>(sbase) +
-                                                     RG_::kKCh * 16);
+        if (i + 2 < nt) issue_tile(kt + 2, std::integral_constant<int, NEXT>{});
+        const unsigned char* st = ring + STAGE * RG_::kStageBytes;
         const int valid = ke - kt * kKeyTile;      // keys of this tile below ke
         if (valid < kKeyTile) {
             // Zero V^T for the keys past ke so 0-weight products stay 0.
+            uint16_t* vlds = reinterpret_cast<uint16_t*>(const_cast<unsigned char*>(st) +
+                                                         RG_::kKCh * 16);
             for (int e = tid; e < D * kKeyTile; e += kAttnThreads) {
                 const int d = e / kKeyTile, key = e % kKeyTile;
                 if (key >= valid) {
@@ -376,14 +444,19 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             }
             barrier_raw();
         }
-
-        // S^T (32 keys x 32 rows) = K Q^T
+        constexpr int PREV = (STAGE + kStages - 1) % kStages;
+        const unsigned char* vprev = ring + PREV * RG_::kStageBytes;
+        const bool have_pv = i > 0;
         floatx16 s = floatx16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const int chunk = (kk * 2 + h) ^ kswz;
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(klds + krow * D + chunk * 8);
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(st + koff[kk]);
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
+            if (have_pv && kk < DT * 2) pv_mfma(vprev, kk >> 1, kk & 1);
+        }
+        if (have_pv) {
+#pragma unroll
+            for (int x = KK; x < DT * 2; ++x) pv_mfma(vprev, x >> 1, x & 1);
         }
         if (valid < kKeyTile) {
 #pragma unroll
@@ -392,9 +465,9 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                 if (key >= valid) s[x] = -INFINITY;
             }
         }
-        float mx = s[0];
+        float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
-        for (int x = 1; x < 16; ++x) mx = fmaxf(mx, s[x]);
+        for (int x = 3; x < 16; x += 2) mx = fmaxf(fmaxf(mx, s[x]), x + 1 < 16 ? s[x + 1] : s[x]);
         mx = wave_xor32_max(mx) * scale_log2;
         const bool need = mx > m_run + kRescaleSlack;
         if (__any(need)) {
@@ -404,30 +477,41 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
                 for (int x = 0; x < 16; ++x) o[dt][x] *= alpha;
-            l_part *= alpha;
+            l_acc[0] *= alpha;
+            l_acc[1] *= alpha;
             m_run = m_new;
         }
-        bf16x8 pb[2];
 #pragma unroll
-        for (int x = 0; x < 16; ++x) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[x], scale_log2, -m_run));
-            l_part += p;
-            pb[x >> 3][x & 7] = (__bf16)p;
+        for (int x = 0; x < 16; ++x)
+            pb[x >> 3][x & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[x], scale_log2, -m_run));
+        // denominator from the same rounded weights the PV product uses
+#pragma unroll
+        for (int x = 0; x < 8; x += 2) {
+            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+            const bf16x2 p0 = {pb[0][x], pb[0][x + 1]};
+            const bf16x2 p1 = {pb[1][x], pb[1][x + 1]};
+            const bf16x2 one2 = {ones[0], ones[1]};
+            l_acc[0] = __builtin_amdgcn_fdot2_f32_bf16(p0, one2, l_acc[0], false);
+            l_acc[1] = __builtin_amdgcn_fdot2_f32_bf16(p1, one2, l_acc[1], false);
         }
-        // O^T (d x 32 rows) += V^T (d x 32 keys) P^T (32 keys x 32 rows)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-            const int d = dt * 32 + n;
-            const int vsw = (d >> 2) & 3;
-#pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-                const int pos = (tt * 2 + h) ^ vsw;
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(vlds + d * kKeyTile + pos * 8);
-                o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[tt], o[dt], 0, 0, 0);
-            }
+    };
+
+    if (nt > 0) {
+        issue_tile(kt0, std::integral_constant<int, 0>{});
+        if (nt > 1) issue_tile(kt0 + 1, std::integral_constant<int, 1>{});
+        for (int i = 0; i < nt; i += kStages) {
+            step(i, std::integral_constant<int, 0>{});
+            if (i + 1 < nt) step(i + 1, std::integral_constant<int, 1>{});
+            if (i + 2 < nt) step(i + 2, std::integral_constant<int, 2>{});
+            if (i + 3 < nt) step(i + 3, std::integral_constant<int, 3>{});
         }
+        // PV of the last tile
+        const unsigned char* vprev = ring + ((nt - 1) % kStages) * RG_::kStageBytes;
+#pragma unroll
+        for (int x = 0; x < DT * 2; ++x) pv_mfma(vprev, x >> 1, x & 1);
     }
 
+    float l_part = l_acc[0] + l_acc[1];
     const float l = l_part + __shfl_xor(l_part, 32, 64);
     const float inv_l = 1.0f / l;
     if (slot < 0) {
