@@ -403,72 +403,79 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     for (int dt = 0; dt < DT; ++dt) o[dt] = floatx16{};
     float m_run = -INFINITY;   // running max of scores, log2 domain
     float l_acc[2] = {0.f, 0.f};   // this lane's share of the denominator
-    bf16x8 pb[2];              // P^T of the previous tile, waiting for its PV
-    const bf16x8 ones = {(__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f,
-                         (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f};
+    bf16x8 pb[2];              // P^T of the current tile (B operand of PV)
 
     const int kt0 = kb / kKeyTile;
     const int nt = (ke + kKeyTile - 1) / kKeyTile - kt0;
+    const int valid_last = ke - (kt0 + nt - 1) * kKeyTile;   // keys of the last tile below ke
+    constexpr int kAhead = KK < 4 ? KK : 4;   // LDS operand reads kept in flight
 
-    auto pv_mfma = [&](const unsigned char* vst, int dt, int tt) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vst + voff[dt][tt]);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[tt], o[dt], 0, 0, 0);
-    };
-
-    // One key tile i: wait for its stage; refill the stage of tile i-2 (free
-    // once every wave has passed this barrier: its PV ran in step i-1) with
-    // tile i+2; then S^T = K Q^T interleaved with the pending O^T += V^T P^T
-    // of tile i-1 (whose stage stays untouched until step i+1); then the
-    // online softmax of tile i.  Stages in use: i-1, i, i+1, i+2.
-    static_assert(kStages == 4, "the refill distance assumes four stages");
-    auto step = [&](int i, auto stage_c) {
-        constexpr int STAGE = decltype(stage_c)::value;
-        constexpr int NEXT = (STAGE + 2) % kStages;
-        const int kt = kt0 + i;
-        if (i + 1 < nt) wait_vm(NCH);    // tile i+1 may still be in flight
-        else wait_vm(0);
-        barrier_raw();
-        if (i + 2 < nt) issue_tile(kt + 2, std::integral_constant<int, NEXT>{});
-        const unsigned char* st = ring + STAGE * RG_::kStageBytes;
-        const int valid = ke - kt * kKeyTile;      // keys of this tile below ke
-        if (valid < kKeyTile) {
-            // Zero V^T for the keys past ke so 0-weight products stay 0.
-            uint16_t* vlds = reinterpret_cast<uint16_t*>(const_cast<unsigned char*>(st) +
-                                                         RG_::kKCh * 16);
-            for (int e = tid; e < D * kKeyTile; e += kAttnThreads) {
-                const int d = e / kKeyTile, key = e % kKeyTile;
-                if (key >= valid) {
-                    const int pos = (key >> 3) ^ ((d >> 2) & 3);
-                    vlds[d * kKeyTile + pos * 8 + (key & 7)] = 0;
-                }
-            }
-            barrier_raw();
-        }
-        constexpr int PREV = (STAGE + kStages - 1) % kStages;
-        const unsigned char* vprev = ring + PREV * RG_::kStageBytes;
-        const bool have_pv = i > 0;
-        floatx16 s = floatx16{};
+    // S^T of one key tile (K fragments from stage kst) into acc.
+    auto s_mfmas = [&](const unsigned char* kst, floatx16& acc) {
+        bf16x8 fr[kAhead];
+#pragma unroll
+        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff[m]);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(st + koff[kk]);
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
-            if (have_pv && kk < DT * 2) pv_mfma(vprev, kk >> 1, kk & 1);
+            const bf16x8 a = fr[kk % kAhead];
+            if (kk + kAhead < KK)
+                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff[kk + kAhead]);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
         }
-        if (have_pv) {
+    };
+    // O^T += V^T P^T of one key tile (V^T fragments from stage vst).
+    auto pv_mfmas = [&](const unsigned char* vst) {
+        constexpr int NX = DT * 2;
+        constexpr int A = NX < 4 ? NX : 4;
+        bf16x8 fr[A];
 #pragma unroll
-            for (int x = KK; x < DT * 2; ++x) pv_mfma(vprev, x >> 1, x & 1);
-        }
-        if (valid < kKeyTile) {
+        for (int x = 0; x < A; ++x)
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x >> 1][x & 1]);
 #pragma unroll
-            for (int x = 0; x < 16; ++x) {
-                const int key = 16 * (x >> 3) + 8 * h + (x & 7);
-                if (key >= valid) s[x] = -INFINITY;
-            }
+        for (int x = 0; x < NX; ++x) {
+            const bf16x8 a = fr[x % A];
+            if (x + A < NX)
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) >> 1][(x + A) & 1]);
+            o[x >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x & 1], o[x >> 1], 0, 0, 0);
         }
+    };
+    // Row max of a score tile in the log2 domain (both lane halves hold
+    // different keys of the same query row).
+    auto tile_max = [&](const floatx16& s) -> float {
         float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
         for (int x = 3; x < 16; x += 2) mx = fmaxf(fmaxf(mx, s[x]), x + 1 < 16 ? s[x + 1] : s[x]);
-        mx = wave_xor32_max(mx) * scale_log2;
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+    };
+    // P^T = exp2(S^T * scale - m) rounded to bf16, and the denominator from
+    // the same rounded weights the PV product uses.
+    auto softmax_p = [&](const floatx16& s) {
+#pragma unroll
+        for (int x = 0; x < 16; ++x)
+            pb[x >> 3][x & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[x], scale_log2, -m_run));
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+        for (int x = 0; x < 8; x += 2) {
+            const bf16x2 p0 = {pb[0][x], pb[0][x + 1]};
+            const bf16x2 p1 = {pb[1][x], pb[1][x + 1]};
+            l_acc[0] = __builtin_amdgcn_fdot2_f32_bf16(p0, one2, l_acc[0], false);
+            l_acc[1] = __builtin_amdgcn_fdot2_f32_bf16(p1, one2, l_acc[1], false);
+        }
+    };
+    // Scores of keys at or past ke (only in the last tile) become -inf.
+    auto mask_tail = [&](floatx16& s) {
+#pragma unroll
+        for (int x = 0; x < 16; ++x) {
+            const int key = 16 * (x >> 3) + 8 * h + (x & 7);
+            if (key >= valid_last) s[x] = -INFINITY;
+        }
+    };
+    // Lazy rescale: move the running max only when a row's tile max passes
+    // it by more than the slack; O and the denominator follow.
+    auto update_max = [&](float mx) {
         const bool need = mx > m_run + kRescaleSlack;
         if (__any(need)) {
             const float m_new = need ? mx : m_run;
@@ -481,34 +488,144 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             l_acc[1] *= alpha;
             m_run = m_new;
         }
+    };
+
+    // Phase 1 of a step: S^T of the next tile (K fragments from kst) on the
+    // matrix core, while the VALU turns the current tile's scores into P^T.
+    // Each group holds one MFMA and a share of the VALU work; scheduling
+    // barriers between groups keep that interleave.
+    auto phase1 = [&](const unsigned char* kst, const floatx16& sc, floatx16& acc) {
+        constexpr int SPG = 16 / KK;   // scores per group
+        static_assert(SPG % 2 == 0, "scores go in pairs");
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+        bf16x8 fr[kAhead];
 #pragma unroll
-        for (int x = 0; x < 16; ++x)
-            pb[x >> 3][x & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[x], scale_log2, -m_run));
-        // denominator from the same rounded weights the PV product uses
+        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff[m]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int x = 0; x < 8; x += 2) {
-            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-            const bf16x2 p0 = {pb[0][x], pb[0][x + 1]};
-            const bf16x2 p1 = {pb[1][x], pb[1][x + 1]};
-            const bf16x2 one2 = {ones[0], ones[1]};
-            l_acc[0] = __builtin_amdgcn_fdot2_f32_bf16(p0, one2, l_acc[0], false);
-            l_acc[1] = __builtin_amdgcn_fdot2_f32_bf16(p1, one2, l_acc[1], false);
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8 a = fr[kk % kAhead];
+            if (kk + kAhead < KK)
+                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff[kk + kAhead]);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
+#pragma unroll
+            for (int y = 0; y < SPG; y += 2) {
+                const int x = kk * SPG + y;
+                const __bf16 p0 = (__bf16)__builtin_amdgcn_exp2f(fmaf(sc[x], scale_log2, -m_run));
+                const __bf16 p1 = (__bf16)__builtin_amdgcn_exp2f(fmaf(sc[x + 1], scale_log2, -m_run));
+                pb[x >> 3][x & 7] = p0;
+                pb[x >> 3][(x & 7) + 1] = p1;
+                const bf16x2 pp = {p0, p1};
+                l_acc[x >> 3] = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_acc[x >> 3], false);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
+    };
+    // Phase 2: O^T += V^T P^T of the current tile (V^T fragments from vst)
+    // while the VALU takes the row max of the next tile's scores.
+    auto phase2 = [&](const unsigned char* vst, const floatx16& sn) -> float {
+        constexpr int NX = DT * 2;
+        constexpr int A = NX < 4 ? NX : 4;
+        constexpr int VPG = 16 / NX;   // scores per group
+        bf16x8 fr[A];
+#pragma unroll
+        for (int x = 0; x < A; ++x)
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x >> 1][x & 1]);
+        float mx = -INFINITY;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int x = 0; x < NX; ++x) {
+            const bf16x8 a = fr[x % A];
+            if (x + A < NX)
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) >> 1][(x + A) & 1]);
+            o[x >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x & 1], o[x >> 1], 0, 0, 0);
+#pragma unroll
+            for (int y = 0; y < VPG; ++y) mx = fmaxf(mx, sn[x * VPG + y]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+    };
+
+    // Software pipeline over key tiles, one step per tile i < nt-1:
+    //   wait for tile i+1 and barrier; refill the stage of tile i-1 (read by
+    //   every wave before this barrier) with tile i+3;
+    //   phase 1: S^T(i+1) on the matrix core while the VALU turns S^T(i)
+    //            into P^T(i);
+    //   phase 2: O^T += V^T(i) P^T(i) while the VALU takes the row max of
+    //            S^T(i+1);
+    //   then the (rare) rescale for tile i+1.
+    // Stages in use: i (V), i+1 (K), i+2 and i+3 in flight.
+    static_assert(kStages == 4, "the refill distance assumes four stages");
+    floatx16 s_cur = floatx16{};
+    auto step = [&](int i, auto stage_c, auto last_c) {
+        constexpr int STAGE = decltype(stage_c)::value;
+        constexpr bool LAST = decltype(last_c)::value;   // tile i+1 is the last one
+        constexpr int NXT = (STAGE + 1) % kStages;
+        constexpr int FREE = (STAGE + 3) % kStages;
+        if (i + 2 < nt) wait_vm(NCH);
+        else wait_vm(0);
+        barrier_raw();
+        if (i + 3 < nt) issue_tile(kt0 + i + 3, std::integral_constant<int, FREE>{});
+        const unsigned char* kst = ring + NXT * RG_::kStageBytes;
+        const unsigned char* vst = ring + STAGE * RG_::kStageBytes;   // V^T offsets include the K part
+
+        floatx16 s_nxt = floatx16{};
+        phase1(kst, s_cur, s_nxt);
+        if constexpr (LAST) {
+            if (valid_last < kKeyTile) mask_tail(s_nxt);
+        }
+        const float mx = phase2(vst, s_nxt);
+        update_max(mx);
+        s_cur = s_nxt;
     };
 
     if (nt > 0) {
         issue_tile(kt0, std::integral_constant<int, 0>{});
         if (nt > 1) issue_tile(kt0 + 1, std::integral_constant<int, 1>{});
-        for (int i = 0; i < nt; i += kStages) {
-            step(i, std::integral_constant<int, 0>{});
-            if (i + 1 < nt) step(i + 1, std::integral_constant<int, 1>{});
-            if (i + 2 < nt) step(i + 2, std::integral_constant<int, 2>{});
-            if (i + 3 < nt) step(i + 3, std::integral_constant<int, 3>{});
+        if (nt > 2) issue_tile(kt0 + 2, std::integral_constant<int, 2>{});
+        wait_vm((nt > 2 ? 2 : nt - 1) * NCH);
+        barrier_raw();
+        s_mfmas(ring, s_cur);
+        if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
+        m_run = tile_max(s_cur);
+        using Mid = std::false_type;
+        using Last = std::true_type;
+        for (int i = 0; i < nt - 2; i += kStages) {
+            step(i, std::integral_constant<int, 0>{}, Mid{});
+            if (i + 1 < nt - 2) step(i + 1, std::integral_constant<int, 1>{}, Mid{});
+            if (i + 2 < nt - 2) step(i + 2, std::integral_constant<int, 2>{}, Mid{});
+            if (i + 3 < nt - 2) step(i + 3, std::integral_constant<int, 3>{}, Mid{});
         }
-        // PV of the last tile
-        const unsigned char* vprev = ring + ((nt - 1) % kStages) * RG_::kStageBytes;
-#pragma unroll
-        for (int x = 0; x < DT * 2; ++x) pv_mfma(vprev, x >> 1, x & 1);
+        // the step that brings in the last tile (which may be partial)
+        if (nt >= 2) {
+            switch ((nt - 2) % kStages) {
+                case 0: step(nt - 2, std::integral_constant<int, 0>{}, Last{}); break;
+                case 1: step(nt - 2, std::integral_constant<int, 1>{}, Last{}); break;
+                case 2: step(nt - 2, std::integral_constant<int, 2>{}, Last{}); break;
+                default: step(nt - 2, std::integral_constant<int, 3>{}, Last{}); break;
+            }
+        }
+        // last tile: P^T, then its PV product
+        softmax_p(s_cur);
+        const int last_stage = (nt - 1) % kStages;
+        unsigned char* slast = ring + last_stage * RG_::kStageBytes;
+        if (valid_last < kKeyTile) {
+            // V^T columns of keys past ke may hold anything (even NaN); zero
+            // them so their 0-weight products stay 0.
+            uint16_t* vlds = reinterpret_cast<uint16_t*>(slast + RG_::kKCh * 16);
+            for (int e = tid; e < D * kKeyTile; e += kAttnThreads) {
+                const int d = e / kKeyTile, key = e % kKeyTile;
+                if (key >= valid_last) {
+                    const int pos = (key >> 3) ^ ((d >> 2) & 3);
+                    vlds[d * kKeyTile + pos * 8 + (key & 7)] = 0;
+                }
+            }
+            barrier_raw();
+        }
+        pv_mfmas(slast);
     }
 
     float l_part = l_acc[0] + l_acc[1];
