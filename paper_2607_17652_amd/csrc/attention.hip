@@ -101,11 +101,17 @@ __device__ inline int unit_key_tiles(const int32_t* tiles, int u, int per_tile,
     return (kv + kKeyTile - 1) / kKeyTile;
 }
 
+// Items are written longest first (a counting sort on their key-tile count,
+// counts of kLenBuckets-1 or more sharing the top bucket): the grid then
+// dispatches long items before short ones, which keeps the tail short.
+constexpr int kLenBuckets = kPlanThreads;
+
 __global__ void __launch_bounds__(kPlanThreads)
 plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             int target_items, int fixed_chunk_tiles, long long max_keys) {
     __shared__ long long sum_lds[kPlanWaves];
     __shared__ int scan_lds[kPlanWaves + 1];
+    __shared__ int bucket[kLenBuckets];
     const int n_tiles = pv.hdr[kHdrTiles];
     const int per_tile = Hkv * RG;
     const int n_units = n_tiles * per_tile;
@@ -138,6 +144,30 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         chunk *= 2;
     }
 
+    // Histogram of item lengths, then each bucket's first position with the
+    // longest bucket first.
+    auto len_key = [&](long long kt, int k) -> int {
+        long long len = kt - (long long)k * chunk;
+        if (len > chunk) len = chunk;
+        return len >= kLenBuckets - 1 ? kLenBuckets - 1 : (int)len;
+    };
+    bucket[threadIdx.x] = 0;
+    __syncthreads();
+    for (int u = threadIdx.x; u < n_units; u += kPlanThreads) {
+        const long long kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+        const int ns = (int)((kt + chunk - 1) / chunk);
+        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kt, k)], 1);
+    }
+    __syncthreads();
+    {
+        const int rev = kLenBuckets - 1 - threadIdx.x;   // descending length order
+        const int cnt = bucket[rev];
+        int total_items;
+        const int first = wg_excl_scan(cnt, scan_lds, &total_items);
+        bucket[rev] = first;
+        __syncthreads();
+    }
+
     int items_before = 0, slots_before = 0;
     for (int base = 0; base < n_units; base += kPlanThreads) {
         const int u = base + threadIdx.x;
@@ -150,7 +180,7 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
                              FB_DERR_PAGE);
         }
         int tot_items, tot_slots;
-        const int item0 = items_before + wg_excl_scan(ns, scan_lds, &tot_items);
+        (void)wg_excl_scan(ns, scan_lds, &tot_items);
         const int slot0 = slots_before + wg_excl_scan(ns > 1 ? ns : 0, scan_lds, &tot_slots);
         if (u < n_units) {
             const int t = u / per_tile;
@@ -158,7 +188,8 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             ws.units[(size_t)u * 2 + kUSplits] = ns;
             ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot0 : -1;
             for (int k = 0; k < ns; ++k) {
-                int32_t* it = ws.items + (size_t)(item0 + k) * 4;
+                const int pos = atomicAdd(&bucket[len_key(kt, k)], 1);
+                int32_t* it = ws.items + (size_t)pos * 4;
                 const long long kb = (long long)k * chunk * kKeyTile;
                 long long ke = kb + chunk * kKeyTile;
                 if (ke > kv) ke = kv;
