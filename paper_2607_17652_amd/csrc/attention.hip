@@ -21,6 +21,7 @@
 //   combine        merges split partials with their log-sum-exp weights
 //   attn_f32       a plain fp32 path (small problems, exactness reference)
 #include <type_traits>
+#include <utility>
 
 #include "internal.h"
 
@@ -225,7 +226,7 @@ __device__ inline float wave_xor32_max(float x) {
     return fmaxf(x, __shfl_xor(x, 32, 64));
 }
 
-// K/V staging: a ring of kStages key tiles in LDS, filled by direct
+// K/V staging: a ring of Ring<D>::kStages key tiles in LDS, filled by direct
 // global->LDS loads (global_load_lds_dwordx4: lane i of a wave writes 16 bytes
 // at M0 + 16*i).  A stage holds the K tile [32 keys][D] followed by the V^T
 // tile [D][32 keys], both in 16-byte chunks whose position inside a row is
@@ -233,10 +234,20 @@ __device__ inline float wave_xor32_max(float x) {
 // the MFMA operand reads of 16 lanes hit 16 distinct bank groups.  The loads
 // are issued from inline asm so the compiler neither sees nor waits on them;
 // the kernel orders them itself with explicit vmcnt waits and raw barriers.
-constexpr int kStages = 4;
+template <int N, typename F, int... I>
+__device__ inline void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+// f(std::integral_constant<int, 0>) ... f(std::integral_constant<int, N-1>)
+template <int N, typename F>
+__device__ inline void static_for(F&& f) {
+    static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
+}
 
 template <int D>
 struct Ring {
+    // Stages of the ring: two workgroups per CU share its 160 KB of LDS.
+    static constexpr int kStages = 4;
     static constexpr int kKCh = kKeyTile * D / 8;   // K chunks per stage
     static constexpr int kVCh = D * kKeyTile / 8;   // V^T chunks per stage
     static constexpr int kCh = kKCh + kVCh;
@@ -277,7 +288,8 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                  uint16_t* __restrict__ out, int Hq, int Hkv, int g, int bl, int RG,
                  int ps, int ps_shift, int max_pages, int num_pages, float scale_log2) {
     using RG_ = Ring<D>;
-    __shared__ __attribute__((aligned(16))) unsigned char ring[kStages * RG_::kStageBytes];
+    constexpr int NS = RG_::kStages;
+    __shared__ __attribute__((aligned(16))) unsigned char ring[NS * RG_::kStageBytes];
     constexpr int KK = D / 16;      // k-steps of the S^T product
     constexpr int DT = D / 32;      // 32-wide d tiles of O^T
     constexpr int NCH = RG_::kPerThread;
@@ -459,15 +471,17 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         constexpr int NX = DT * 2;
         constexpr int A = NX < 4 ? NX : 4;
         bf16x8 fr[A];
+        // product x: d tile x % DT, key half x / DT (consecutive products
+        // accumulate into different tiles)
 #pragma unroll
         for (int x = 0; x < A; ++x)
-            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x >> 1][x & 1]);
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x % DT][x / DT]);
 #pragma unroll
         for (int x = 0; x < NX; ++x) {
             const bf16x8 a = fr[x % A];
             if (x + A < NX)
-                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) >> 1][(x + A) & 1]);
-            o[x >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x & 1], o[x >> 1], 0, 0, 0);
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) % DT][(x + A) / DT]);
+            o[x % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x / DT], o[x % DT], 0, 0, 0);
         }
     };
     // Row max of a score tile in the log2 domain (both lane halves hold
@@ -562,15 +576,15 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         bf16x8 fr[A];
 #pragma unroll
         for (int x = 0; x < A; ++x)
-            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x >> 1][x & 1]);
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x % DT][x / DT]);
         float mx = -INFINITY;
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int x = 0; x < NX; ++x) {
             const bf16x8 a = fr[x % A];
             if (x + A < NX)
-                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) >> 1][(x + A) & 1]);
-            o[x >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x & 1], o[x >> 1], 0, 0, 0);
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) % DT][(x + A) / DT]);
+            o[x % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x / DT], o[x % DT], 0, 0, 0);
 #pragma unroll
             for (int y = 0; y < VPG; ++y) mx = fmaxf(mx, sn[x * VPG + y]);
             __builtin_amdgcn_sched_barrier(0);
@@ -582,24 +596,25 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 
     // Software pipeline over key tiles, one step per tile i < nt-1:
     //   wait for tile i+1 and barrier; refill the stage of tile i-1 (read by
-    //   every wave before this barrier) with tile i+3;
+    //   every wave before this barrier) with tile i+NS-1;
     //   phase 1: S^T(i+1) on the matrix core while the VALU turns S^T(i)
     //            into P^T(i);
     //   phase 2: O^T += V^T(i) P^T(i) while the VALU takes the row max of
     //            S^T(i+1);
     //   then the (rare) rescale for tile i+1.
-    // Stages in use: i (V), i+1 (K), i+2 and i+3 in flight.
-    static_assert(kStages == 4, "the refill distance assumes four stages");
+    // Stages in use: i (V), i+1 (K), i+2 .. i+NS-1 in flight.
+    static_assert(NS >= 3, "the ring needs the current, next and one loading stage");
     floatx16 s_cur = floatx16{};
     auto step = [&](int i, auto stage_c, auto last_c) {
         constexpr int STAGE = decltype(stage_c)::value;
         constexpr bool LAST = decltype(last_c)::value;   // tile i+1 is the last one
-        constexpr int NXT = (STAGE + 1) % kStages;
-        constexpr int FREE = (STAGE + 3) % kStages;
-        if (i + 2 < nt) wait_vm(NCH);
-        else wait_vm(0);
+        constexpr int NXT = (STAGE + 1) % NS;
+        constexpr int FREE = (STAGE + NS - 1) % NS;
+        int behind = nt - 2 - i;            // tiles issued after tile i+1
+        if (behind > NS - 3) behind = NS - 3;
+        wait_vm(behind * NCH);
         barrier_raw();
-        if (i + 3 < nt) issue_tile(kt0 + i + 3, std::integral_constant<int, FREE>{});
+        if (i + NS - 1 < nt) issue_tile(kt0 + i + NS - 1, std::integral_constant<int, FREE>{});
         const unsigned char* kst = ring + NXT * RG_::kStageBytes;
         const unsigned char* vst = ring + STAGE * RG_::kStageBytes;   // V^T offsets include the K part
 
@@ -614,34 +629,31 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     };
 
     if (nt > 0) {
-        issue_tile(kt0, std::integral_constant<int, 0>{});
-        if (nt > 1) issue_tile(kt0 + 1, std::integral_constant<int, 1>{});
-        if (nt > 2) issue_tile(kt0 + 2, std::integral_constant<int, 2>{});
-        wait_vm((nt > 2 ? 2 : nt - 1) * NCH);
+        static_for<NS - 1>([&](auto j) {
+            if (j < nt) issue_tile(kt0 + j, j);
+        });
+        wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
         barrier_raw();
         s_mfmas(ring, s_cur);
         if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
         m_run = tile_max(s_cur);
         using Mid = std::false_type;
         using Last = std::true_type;
-        for (int i = 0; i < nt - 2; i += kStages) {
-            step(i, std::integral_constant<int, 0>{}, Mid{});
-            if (i + 1 < nt - 2) step(i + 1, std::integral_constant<int, 1>{}, Mid{});
-            if (i + 2 < nt - 2) step(i + 2, std::integral_constant<int, 2>{}, Mid{});
-            if (i + 3 < nt - 2) step(i + 3, std::integral_constant<int, 3>{}, Mid{});
+        for (int i = 0; i < nt - 2; i += NS) {
+            static_for<NS>([&](auto j) {
+                if (i + j < nt - 2) step(i + j, j, Mid{});
+            });
         }
         // the step that brings in the last tile (which may be partial)
         if (nt >= 2) {
-            switch ((nt - 2) % kStages) {
-                case 0: step(nt - 2, std::integral_constant<int, 0>{}, Last{}); break;
-                case 1: step(nt - 2, std::integral_constant<int, 1>{}, Last{}); break;
-                case 2: step(nt - 2, std::integral_constant<int, 2>{}, Last{}); break;
-                default: step(nt - 2, std::integral_constant<int, 3>{}, Last{}); break;
-            }
+            const int st2 = (nt - 2) % NS;
+            static_for<NS>([&](auto j) {
+                if (st2 == j) step(nt - 2, j, Last{});
+            });
         }
         // last tile: P^T, then its PV product
         softmax_p(s_cur);
-        const int last_stage = (nt - 1) % kStages;
+        const int last_stage = (nt - 1) % NS;
         unsigned char* slast = ring + last_stage * RG_::kStageBytes;
         if (valid_last < kKeyTile) {
             // V^T columns of keys past ke may hold anything (even NaN); zero
@@ -703,58 +715,73 @@ __device__ inline void store_out<uint16_t>(uint16_t* p, float v) {
 template <>
 __device__ inline void store_out<float>(float* p, float v) { *p = v; }
 
-// One workgroup per split unit: the per-split log-sum-exp weights of each
-// row are computed once into LDS, then every thread merges 4 consecutive d
-// of a row with 16-byte loads.
-constexpr int kMaxSplitsLds = kMaxSplits;
+// Each split unit's rows are merged by kCombineParts workgroups of
+// kCombineRows rows: a row's per-split log-sum-exp weights go to LDS once,
+// then every thread merges 16-byte columns of its rows, four splits' loads
+// in flight at a time.
+constexpr int kCombineRows = 32;
+constexpr int kCombineParts = kRowsPerWg / kCombineRows;
 
 template <typename T>
 __global__ void __launch_bounds__(kAttnThreads)
 combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
                int g, int bl, int RG, int D) {
-    __shared__ float wgt[kMaxSplitsLds][kRowsPerWg];
-    __shared__ float inv_den[kRowsPerWg];
-    const int u = blockIdx.x;
+    __shared__ float wgt[kMaxSplits][kCombineRows];
+    __shared__ float inv_den[kCombineRows];
+    const int u = blockIdx.x / kCombineParts;
+    const int part = blockIdx.x % kCombineParts;
     if (u >= ws.counts[kCUnits]) return;
-    const int ns = ws.units[(size_t)u * 2 + kUSplits];
+    const int ns = ws.units[(size_t)u * 2 + kUSplits];   // <= kMaxSplits (plan)
     if (ns <= 1) return;
     const int slot0 = ws.units[(size_t)u * 2 + kUSlot0];
     const int rg = u % RG;
     const int c = (u / RG) % Hkv;
     const int t = u / (RG * Hkv);
     const int row0 = pv.tiles[(size_t)t * kTileInts + kTRow0];
-    const int nrows = min(kRowsPerWg, bl * g - rg * kRowsPerWg);
-    const int nsl = min(ns, kMaxSplitsLds);
-    for (int rl = threadIdx.x; rl < nrows; rl += kAttnThreads) {
+    const int rbase = part * kCombineRows;
+    const int nrows = min(kCombineRows, bl * g - rg * kRowsPerWg - rbase);
+    if (nrows <= 0) return;
+    if (threadIdx.x < nrows) {
+        const float* lse = ws.part_lse + (size_t)slot0 * kRowsPerWg + rbase + threadIdx.x;
         float mx = -INFINITY;
-        for (int k = 0; k < ns; ++k)
-            mx = fmaxf(mx, ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl]);
+        for (int k = 0; k < ns; ++k) mx = fmaxf(mx, lse[(size_t)k * kRowsPerWg]);
         float den = 0.f;
         for (int k = 0; k < ns; ++k) {
-            const float w = __builtin_amdgcn_exp2f(
-                ws.part_lse[(size_t)(slot0 + k) * kRowsPerWg + rl] - mx);
-            if (k < nsl) wgt[k][rl] = w;
+            const float w = __builtin_amdgcn_exp2f(lse[(size_t)k * kRowsPerWg] - mx);
+            wgt[k][threadIdx.x] = w;
             den += w;
         }
-        inv_den[rl] = 1.0f / den;
+        inv_den[threadIdx.x] = 1.0f / den;
     }
     __syncthreads();
     const int per_row = D / 4;
+    const size_t stride = (size_t)kRowsPerWg * D;   // one split's partial O
     for (int e = threadIdx.x; e < nrows * per_row; e += kAttnThreads) {
-        const int rl = e / per_row;
+        const int rr = e / per_row;
         const int d0 = (e % per_row) * 4;
+        const float* src = ws.part_o + ((size_t)slot0 * kRowsPerWg + rbase + rr) * D + d0;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int k = 0; k < nsl; ++k) {
-            const float w = wgt[k][rl];
-            const float4 v = *reinterpret_cast<const float4*>(
-                ws.part_o + ((size_t)(slot0 + k) * kRowsPerWg + rl) * D + d0);
+        auto add = [&](float w, const float4& v) {
             acc.x += w * v.x;
             acc.y += w * v.y;
             acc.z += w * v.z;
             acc.w += w * v.w;
+        };
+        int k = 0;
+        for (; k + 4 <= ns; k += 4) {
+            const float4 v0 = *reinterpret_cast<const float4*>(src + (size_t)k * stride);
+            const float4 v1 = *reinterpret_cast<const float4*>(src + (size_t)(k + 1) * stride);
+            const float4 v2 = *reinterpret_cast<const float4*>(src + (size_t)(k + 2) * stride);
+            const float4 v3 = *reinterpret_cast<const float4*>(src + (size_t)(k + 3) * stride);
+            add(wgt[k][rr], v0);
+            add(wgt[k + 1][rr], v1);
+            add(wgt[k + 2][rr], v2);
+            add(wgt[k + 3][rr], v3);
         }
-        const float id = inv_den[rl];
-        const int r = rg * kRowsPerWg + rl;
+        for (; k < ns; ++k)
+            add(wgt[k][rr], *reinterpret_cast<const float4*>(src + (size_t)k * stride));
+        const float id = inv_den[rr];
+        const int r = rg * kRowsPerWg + rbase + rr;
         const int pos_local = r / g, hg = r % g;
         T* dst = out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d0;
         store_out<T>(dst + 0, acc.x * id);
@@ -949,7 +976,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.unit_cap), dim3(kAttnThreads),
+    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.unit_cap * kCombineParts), dim3(kAttnThreads),
                        0, stream, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl,
                        z.row_groups, sh->head_dim);
     return hipGetLastError();
