@@ -93,10 +93,9 @@ __device__ int wg_excl_scan(int v, int* lds, int* total) {
     return excl;
 }
 
-// Key tiles of unit u; 0 (skip) when its keys run past the page table.
-__device__ inline int unit_key_tiles(const int32_t* tiles, int u, int per_tile,
-                                     long long max_keys) {
-    const int t = u / per_tile;
+// Key tiles of tile t (every unit of a tile has the same key range); 0 (skip)
+// when its keys run past the page table.
+__device__ inline int tile_key_tiles(const int32_t* tiles, int t, long long max_keys) {
     const int kv = tiles[(size_t)t * kTileInts + kTKvLen];
     if ((long long)kv > max_keys) return 0;
     return (kv + kKeyTile - 1) / kKeyTile;
@@ -104,7 +103,9 @@ __device__ inline int unit_key_tiles(const int32_t* tiles, int u, int per_tile,
 
 // Items are written longest first (a counting sort on their key-tile count,
 // counts of kLenBuckets-1 or more sharing the top bucket): the grid then
-// dispatches long items before short ones, which keeps the tail short.
+// dispatches long items before short ones, which keeps the tail short.  The
+// plan works per tile: the per_tile units of a tile (kv-heads x row groups)
+// have the same key range, so they get the same split and adjacent items.
 constexpr int kLenBuckets = kPlanThreads;
 
 __global__ void __launch_bounds__(kPlanThreads)
@@ -118,9 +119,9 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     const int n_units = n_tiles * per_tile;
 
     long long my_tiles = 0;
-    for (int u = threadIdx.x; u < n_units; u += kPlanThreads)
-        my_tiles += unit_key_tiles(pv.tiles, u, per_tile, max_keys);
-    const long long total_tiles = wg_sum_ll(my_tiles, sum_lds);
+    for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads)
+        my_tiles += tile_key_tiles(pv.tiles, t, max_keys);
+    const long long total_tiles = wg_sum_ll(my_tiles, sum_lds) * per_tile;
 
     long long chunk = fixed_chunk_tiles;
     if (chunk <= 0) {
@@ -131,11 +132,11 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     // has more splits than the combine merges.
     for (;;) {
         long long my_items = 0, my_slots = 0, my_over = 0;
-        for (int u = threadIdx.x; u < n_units; u += kPlanThreads) {
-            const long long kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+        for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads) {
+            const long long kt = tile_key_tiles(pv.tiles, t, max_keys);
             const long long ns = (kt + chunk - 1) / chunk;
-            my_items += ns;
-            if (ns > 1) my_slots += ns;
+            my_items += ns * per_tile;
+            if (ns > 1) my_slots += ns * per_tile;
             if (ns > kMaxSplits) my_over += 1;
         }
         const long long items = wg_sum_ll(my_items, sum_lds);
@@ -154,10 +155,10 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     };
     bucket[threadIdx.x] = 0;
     __syncthreads();
-    for (int u = threadIdx.x; u < n_units; u += kPlanThreads) {
-        const long long kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+    for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads) {
+        const long long kt = tile_key_tiles(pv.tiles, t, max_keys);
         const int ns = (int)((kt + chunk - 1) / chunk);
-        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kt, k)], 1);
+        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kt, k)], per_tile);
     }
     __syncthreads();
     {
@@ -170,34 +171,37 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     }
 
     int items_before = 0, slots_before = 0;
-    for (int base = 0; base < n_units; base += kPlanThreads) {
-        const int u = base + threadIdx.x;
-        int ns = 0, kt = 0;
-        if (u < n_units) {
-            kt = unit_key_tiles(pv.tiles, u, per_tile, max_keys);
+    for (int base = 0; base < n_tiles; base += kPlanThreads) {
+        const int t = base + threadIdx.x;
+        int ns = 0, kt = 0, kv = 0;
+        if (t < n_tiles) {
+            kt = tile_key_tiles(pv.tiles, t, max_keys);
+            kv = pv.tiles[(size_t)t * kTileInts + kTKvLen];
             ns = (int)((kt + chunk - 1) / chunk);
-            if (kt == 0)
-                record_error(pv.hdr, pv.tiles[(size_t)(u / per_tile) * kTileInts + kTB],
-                             FB_DERR_PAGE);
+            if (kt == 0) record_error(pv.hdr, pv.tiles[(size_t)t * kTileInts + kTB], FB_DERR_PAGE);
         }
         int tot_items, tot_slots;
-        (void)wg_excl_scan(ns, scan_lds, &tot_items);
-        const int slot0 = slots_before + wg_excl_scan(ns > 1 ? ns : 0, scan_lds, &tot_slots);
-        if (u < n_units) {
-            const int t = u / per_tile;
-            const int kv = pv.tiles[(size_t)t * kTileInts + kTKvLen];
-            ws.units[(size_t)u * 2 + kUSplits] = ns;
-            ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot0 : -1;
+        (void)wg_excl_scan(ns * per_tile, scan_lds, &tot_items);
+        const int slot_t = slots_before + wg_excl_scan(ns > 1 ? ns * per_tile : 0, scan_lds, &tot_slots);
+        if (t < n_tiles) {
+            // unit j of the tile owns slots slot_t + j*ns .. + ns-1
+            for (int j = 0; j < per_tile; ++j) {
+                const int u = t * per_tile + j;
+                ws.units[(size_t)u * 2 + kUSplits] = ns;
+                ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot_t + j * ns : -1;
+            }
             for (int k = 0; k < ns; ++k) {
-                const int pos = atomicAdd(&bucket[len_key(kt, k)], 1);
-                int32_t* it = ws.items + (size_t)pos * 4;
+                const int pos = atomicAdd(&bucket[len_key(kt, k)], per_tile);
                 const long long kb = (long long)k * chunk * kKeyTile;
                 long long ke = kb + chunk * kKeyTile;
                 if (ke > kv) ke = kv;
-                it[kIUnit] = u;
-                it[kIKb] = (int)kb;
-                it[kIKe] = (int)ke;
-                it[kISlot] = ns > 1 ? slot0 + k : -1;
+                for (int j = 0; j < per_tile; ++j) {
+                    int32_t* it = ws.items + (size_t)(pos + j) * 4;
+                    it[kIUnit] = t * per_tile + j;
+                    it[kIKb] = (int)kb;
+                    it[kIKe] = (int)ke;
+                    it[kISlot] = ns > 1 ? slot_t + j * ns + k : -1;
+                }
             }
         }
         items_before += tot_items;

@@ -1,8 +1,11 @@
 // Window KV write-back, Eq. 6 (Sec. 4.2, "KV retrieval and write-back"):
 // the fresh K/V of each live block lands at its absolute positions of the
 // paged caches.  One workgroup per (tile, KV head).  K rows are copied in
-// 16-byte vectors; V is staged through LDS and written key-innermost
-// ([page][head][d][slot]) with consecutive lanes on consecutive slots.
+// 16-byte vectors.  V is written key-innermost ([page][head][d][slot]): when
+// the block starts on a 16-byte slot boundary each thread gathers one
+// 16-byte run of slots for one d and stores it whole (neighbouring lanes
+// fill neighbouring runs of the same d row); otherwise V is staged through
+// LDS and stored element by element.
 #include "internal.h"
 
 namespace fb {
@@ -29,14 +32,12 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
     constexpr int VEC = 16 / sizeof(T);
     const int dch = D / VEC;
 
-    // K: straight 16-byte copies; V: rows into LDS.
+    // K: straight 16-byte copies.
     for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
         const int i = e / dch;
         const int dc = e % dch;
         const int pos = pos0 + i;
         const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
-        const uint4 vv = *reinterpret_cast<const uint4*>(v_new + src);
-        *reinterpret_cast<uint4*>(vs + (size_t)i * D + dc * VEC) = vv;
         const int pidx = pos / ps;
         const int page = pidx < max_pages ? pt[pidx] : -1;
         if (page < 0 || page >= num_pages) {
@@ -47,6 +48,36 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
                            (size_t)dc * VEC;
         *reinterpret_cast<uint4*>(k_cache + dst) =
             *reinterpret_cast<const uint4*>(k_new + src);
+    }
+    if (pos0 % VEC == 0 && ps % VEC == 0 && bl % VEC == 0) {
+        // V: run ic of VEC slots for dimension d; lanes walk the runs of a d
+        // row first, so a wave stores whole d rows of the page.
+        const int nrun = bl / VEC;
+        for (int e = threadIdx.x; e < D * nrun; e += kKvThreads) {
+            const int ic = e % nrun;
+            const int d = e / nrun;
+            const int pos = pos0 + ic * VEC;
+            const int pidx = pos / ps;
+            const int page = pidx < max_pages ? pt[pidx] : -1;
+            if (page < 0 || page >= num_pages) continue;   // recorded by the K loop
+            union {
+                uint4 v;
+                T x[VEC];
+            } run;
+#pragma unroll
+            for (int k = 0; k < VEC; ++k)
+                run.x[k] = v_new[((size_t)(row0 + ic * VEC + k) * Hkv + c) * D + d];
+            *reinterpret_cast<uint4*>(v_cache + (((size_t)page * Hkv + c) * D + d) * ps +
+                                      (pos % ps)) = run.v;
+        }
+        return;
+    }
+    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
+        const int i = e / dch;
+        const int dc = e % dch;
+        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
+        *reinterpret_cast<uint4*>(vs + (size_t)i * D + dc * VEC) =
+            *reinterpret_cast<const uint4*>(v_new + src);
     }
     __syncthreads();
     for (int e = threadIdx.x; e < bl * D; e += kKvThreads) {

@@ -1,12 +1,12 @@
-// Heterogeneous Wavefront Packing, Eq. 4 (Sec. 4.2): one workgroup turns the
-// per-request wavefront states into the packed batch -- a compact list of
-// live-block tiles plus per-row request / position / token maps.
+// Heterogeneous Wavefront Packing, Eq. 4 (Sec. 4.2): the per-request
+// wavefront states become the packed batch -- a compact list of live-block
+// tiles plus per-row request / position / token maps.
 //
-// Phase 1 validates every request and computes w_b; a block-wide exclusive
-// scan of w_b gives each request its first tile (and, in the ragged layout,
-// its first packed row).  Phase 2 writes every one of the row_cap row-map
-// entries exactly once, live or not, so the output is fully defined without
-// a separate clearing pass.
+// pack_kernel (one workgroup) validates every request and computes w_b; a
+// block-wide exclusive scan of w_b gives each request its first tile (and, in
+// the ragged layout, its first packed row).  rowmap_kernel then writes every
+// one of the row_cap row-map entries exactly once, live or not, so the output
+// is fully defined without a separate clearing pass.
 #include "internal.h"
 
 namespace fb {
@@ -94,36 +94,42 @@ pack_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tok
         }
         tiles_before += total;
     }
-    const int n_tiles = tiles_before;
-    const int n_rows = n_tiles * bl;
-    __syncthreads();
-
-    // ---- phase 2: every row-map entry, written once ------------------------
-    const int q = W_max * bl;
-    for (int r = tid; r < row_cap; r += kPackThreads) {
-        int b = -1, pos = -1;
-        if (layout == FB_PADDED) {
-            const int rb = r / q;
-            const int slot = (r % q) / bl;
-            const int w = pv.req_w[rb];
-            if (slot < w) {
-                const fb_req_state s = st[rb];
-                b = rb;
-                pos = s.gen_start + s.L * bl + (r % q);
-            }
-        } else if (r < n_rows) {
-            const int32_t* t = pv.tiles + (size_t)(r / bl) * kTileInts;
-            b = t[kTB];
-            pos = t[kTPos0] + (r % bl);
-        }
-        pv.row_req[r] = b;
-        pv.row_pos[r] = pos;
-        pv.row_tok[r] = (b >= 0 && tokens) ? tokens[(size_t)b * T_max + pos] : -1;
-    }
     if (tid == 0) {
-        pv.hdr[kHdrRows] = n_rows;
-        pv.hdr[kHdrTiles] = n_tiles;
+        pv.hdr[kHdrRows] = tiles_before * bl;
+        pv.hdr[kHdrTiles] = tiles_before;
     }
+}
+
+// Row maps (row -> request, position, token), one thread per packed row.
+// Ragged rows are tile-major (row r belongs to tile r / bl); padded rows
+// belong to request r / (W_max*bl).
+constexpr int kRowThreads = 256;
+
+__global__ void __launch_bounds__(kRowThreads)
+rowmap_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tokens,
+              int W_max, int bl, int layout, int T_max, PackView pv, int row_cap) {
+    const int r = blockIdx.x * kRowThreads + threadIdx.x;
+    if (r >= row_cap) return;
+    const int n_rows = pv.hdr[kHdrRows];
+    const int q = W_max * bl;
+    int b = -1, pos = -1;
+    if (layout == FB_PADDED) {
+        const int rb = r / q;
+        const int slot = (r % q) / bl;
+        const int w = pv.req_w[rb];
+        if (slot < w) {
+            const fb_req_state s = st[rb];
+            b = rb;
+            pos = s.gen_start + s.L * bl + (r % q);
+        }
+    } else if (r < n_rows) {
+        const int32_t* t = pv.tiles + (size_t)(r / bl) * kTileInts;
+        b = t[kTB];
+        pos = t[kTPos0] + (r % bl);
+    }
+    pv.row_req[r] = b;
+    pv.row_pos[r] = pos;
+    pv.row_tok[r] = (b >= 0 && tokens) ? tokens[(size_t)b * T_max + pos] : -1;
 }
 
 }  // namespace
@@ -134,6 +140,11 @@ hipError_t launch_pack(const fb_req_state* st, const int32_t* tokens, int n_max,
     hipLaunchKernelGGL(pack_kernel, dim3(1), dim3(kPackThreads), 0, stream, st,
                        tokens, pack->B, pack->W_max, pack->bl, pack->layout,
                        n_max, T_max, pv, pack->row_cap);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(rowmap_kernel, dim3((pack->row_cap + kRowThreads - 1) / kRowThreads),
+                       dim3(kRowThreads), 0, stream, st, tokens, pack->W_max, pack->bl,
+                       pack->layout, T_max, pv, pack->row_cap);
     return hipGetLastError();
 }
 
