@@ -79,6 +79,16 @@ __device__ inline void top_fold(Top& t, const float (&f)[N], int v) {
     t.s += e[0];
 }
 
+// 16-byte load of logits that are read exactly once: the nontemporal hint
+// keeps the stream from displacing reusable lines in the caches, which
+// measurably raises the achieved HBM read rate of this pass.
+template <typename T>
+__device__ inline uint4 load_stream16(const T* p) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(x[0], x[1], x[2], x[3]);
+}
+
 template <typename T>
 struct VecTraits;
 template <>
@@ -141,7 +151,7 @@ vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             const int v = base + j * stride;
-            raw[j] = v < e ? *reinterpret_cast<const uint4*>(rp + v) : make_uint4(0, 0, 0, 0);
+            raw[j] = v < e ? load_stream16(rp + v) : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
