@@ -39,6 +39,8 @@ def parse_args():
     ap.add_argument("--workload", default="serve256")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the HIP-graph replay of the K steps")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
@@ -185,6 +187,45 @@ def cpu_baseline(wl, host, t, budget_s, seed):
                       f"threads, the rest on one"}
 
 
+def graph_replay(torch, fb, step, one_step, copies, K, W):
+    """The same K steps captured once in a HIP graph and replayed.
+
+    Each captured step works on its own pristine copy of the request state,
+    as in the eager loop.  A warm-up replay runs first, the copies are
+    restored outside the graph, then one timed replay.  Its outputs (last
+    step's attention output, confidences, argmax, stats and updated state)
+    must equal the eager ones bit for bit, else the figure is withheld."""
+    ref = [x.clone() for x in copies[K]] + [step.out.clone(), step.conf.clone(),
+                                           step.argmax.clone(), step.stats.clone()]
+    pristine = (step.st, step.tokens, step.pe, step.fin)
+    gcopies = [tuple(x.clone() for x in pristine) for _ in range(K)]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(K):
+            one_step(0, None, gcopies[i])
+
+    def restore():
+        for c in gcopies:
+            for dst, src in zip(c, pristine):
+                dst.copy_(src)
+        torch.cuda.synchronize()
+
+    g.replay()
+    restore()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    got = list(gcopies[0]) + [step.out, step.conf, step.argmax, step.stats]
+    same = all(torch.equal(a, b) for a, b in zip(got, ref)) and \
+        all(torch.equal(a, b) for a, b in zip(gcopies[K - 1], ref[:4]))
+    return {"ms_per_step": ms if same else None, "matches_eager": bool(same),
+            "steps_per_replay": K}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -218,8 +259,8 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)]
               for _ in range(K)]
 
-    def one_step(i, ev):
-        st, tok, pe, fin = copies[i]
+    def one_step(i, ev, state=None):
+        st, tok, pe, fin = copies[i] if state is None else state
         if ev is not None:
             ev[0].record()
         fb.fb_pack_wavefronts(st, tok, step.n_max, step.T_max, step.pack)
@@ -257,6 +298,7 @@ def main():
     ph = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1])
                             for i in range(K)])) for j, n in enumerate(names)}
     ms_step = wall * 1e3 / K
+    graph = None if args.no_graph else graph_replay(torch, fb, step, one_step, copies, K, W)
     t_attn = ph["attention"] * 1e-3
     t_voc = ph["vocab_reduce"] * 1e-3
     t_upd = (ph["vocab_reduce"] + ph["update_apply"]) * 1e-3
@@ -296,6 +338,8 @@ def main():
         "roofline": dominant,
         "roofline_other": other,
     }
+    if graph is not None:
+        out["graph"] = graph
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
