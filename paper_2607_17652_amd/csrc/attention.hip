@@ -359,6 +359,11 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             ch_off[j] = (uint32_t)(d * ps + kc * 8) * 2u;
         }
     }
+    // Which loads fetch K is wave-uniform; make it scalar so the choice of
+    // base pointer is a scalar select, not a divergent branch.
+    bool ld_isk[NCH];
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) ld_isk[j] = __builtin_amdgcn_readfirstlane((int)ch_isk[j]) != 0;
     uint32_t m0_base[NCH];
     const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0];
 #pragma unroll
@@ -386,12 +391,15 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     }
 
     // Issue the loads of key tile kt into stage STAGE.
-    auto issue_tile = [&](int kt, auto stage_c) {
+    // Page id of key tile kt when a page holds whole tiles (ps >= kKeyTile);
+    // loaded one step before the tile is issued so the scalar load's latency
+    // is off the path.
+    auto tile_page = [&](int kt) -> int { return pt[(kt * kKeyTile) >> ps_shift]; };
+    auto issue_tile = [&](int kt, auto stage_c, int page) {
         constexpr int STAGE = decltype(stage_c)::value;
         const int key0 = kt * kKeyTile;
         if (ps >= kKeyTile) {
             // one page per tile: uniform base + per-lane constant offsets
-            int page = pt[key0 >> ps_shift];
             if (page < 0 || page >= num_pages) {
                 record_error(pv.hdr, b, FB_DERR_PAGE);
                 page = 0;
@@ -402,12 +410,9 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 #pragma unroll
             for (int j = 0; j < NCH; ++j) {
                 const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
-                if (ch_isk[j])
-                    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-                                 :: "s"(m0), "v"(ch_off[j]), "s"(kbase) : "memory");
-                else
-                    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-                                 :: "s"(m0), "v"(ch_off[j]), "s"(vbase) : "memory");
+                const uint16_t* base = ld_isk[j] ? kbase : vbase;
+                asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                             :: "s"(m0), "v"(ch_off[j]), "s"(base) : "memory");
             }
         } else {
             // several pages per tile: per-lane page selection
@@ -609,6 +614,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // Stages in use: i (V), i+1 (K), i+2 .. i+NS-1 in flight.
     static_assert(NS >= 3, "the ring needs the current, next and one loading stage");
     floatx16 s_cur = floatx16{};
+    int pg_next = (ps >= kKeyTile && NS - 1 < nt) ? tile_page(kt0 + NS - 1) : 0;
     auto step = [&](int i, auto stage_c, auto last_c) {
         constexpr int STAGE = decltype(stage_c)::value;
         constexpr bool LAST = decltype(last_c)::value;   // tile i+1 is the last one
@@ -618,7 +624,10 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         if (behind > NS - 3) behind = NS - 3;
         wait_vm(behind * NCH);
         barrier_raw();
-        if (i + NS - 1 < nt) issue_tile(kt0 + i + NS - 1, std::integral_constant<int, FREE>{});
+        if (i + NS - 1 < nt) {
+            issue_tile(kt0 + i + NS - 1, std::integral_constant<int, FREE>{}, pg_next);
+            if (ps >= kKeyTile && i + NS < nt) pg_next = tile_page(kt0 + i + NS);
+        }
         const unsigned char* kst = ring + NXT * RG_::kStageBytes;
         const unsigned char* vst = ring + STAGE * RG_::kStageBytes;   // V^T offsets include the K part
 
@@ -634,7 +643,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 
     if (nt > 0) {
         static_for<NS - 1>([&](auto j) {
-            if (j < nt) issue_tile(kt0 + j, j);
+            if (j < nt) issue_tile(kt0 + j, j, ps >= kKeyTile ? tile_page(kt0 + j) : 0);
         });
         wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
         barrier_raw();
