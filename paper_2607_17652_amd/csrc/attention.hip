@@ -105,7 +105,9 @@ __device__ inline int tile_key_tiles(const int32_t* tiles, int t, long long max_
 // counts of kLenBuckets-1 or more sharing the top bucket): the grid then
 // dispatches long items before short ones, which keeps the tail short.  The
 // plan works per tile: the per_tile units of a tile (kv-heads x row groups)
-// have the same key range, so they get the same split and adjacent items.
+// have the same key range, so they get the same split and adjacent items
+// (with 8 kv-heads the round-robin dispatch then keeps each kv-head on one
+// XCD).
 constexpr int kLenBuckets = kPlanThreads;
 
 __global__ void __launch_bounds__(kPlanThreads)
@@ -153,12 +155,25 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         if (len > chunk) len = chunk;
         return len >= kLenBuckets - 1 ? kLenBuckets - 1 : (int)len;
     };
+    // Sort key of a tile's items: the key tiles of its request's longest
+    // (last) live block, so the blocks of one request, which read the same
+    // prefix K/V, land in the same buckets next to each other and run
+    // together (sharing the prefix through L2) even when many requests have
+    // equal lengths.
+    auto sort_tiles = [&](int t, long long kt) -> long long {
+        const int32_t* tl = pv.tiles + (size_t)t * kTileInts;
+        const long long blen = tl[kTKvLen] - tl[kTPos0];
+        const long long kv_last = tl[kTO] + (long long)tl[kTW] * blen;
+        const long long kr = (kv_last + kKeyTile - 1) / kKeyTile;
+        return kr > kt ? kr : kt;
+    };
     bucket[threadIdx.x] = 0;
     __syncthreads();
     for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads) {
         const long long kt = tile_key_tiles(pv.tiles, t, max_keys);
         const int ns = (int)((kt + chunk - 1) / chunk);
-        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kt, k)], per_tile);
+        const long long kr = sort_tiles(t, kt);
+        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kr, k)], per_tile);
     }
     __syncthreads();
     {
@@ -190,8 +205,9 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
                 ws.units[(size_t)u * 2 + kUSplits] = ns;
                 ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot_t + j * ns : -1;
             }
+            const long long kr = sort_tiles(t, kt);
             for (int k = 0; k < ns; ++k) {
-                const int pos = atomicAdd(&bucket[len_key(kt, k)], per_tile);
+                const int pos = atomicAdd(&bucket[len_key(kr, k)], per_tile);
                 const long long kb = (long long)k * chunk * kKeyTile;
                 long long ke = kb + chunk * kKeyTile;
                 if (ke > kv) ke = kv;
