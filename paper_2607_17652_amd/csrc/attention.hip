@@ -300,7 +300,9 @@ __device__ inline void wait_vm(int n) {
     }
 }
 
-template <int D>
+// FAST: pages hold whole key tiles (page_size >= 32), so a tile's loads share
+// one scalar base; otherwise each lane picks its page.
+template <int D, bool FAST>
 __global__ void __launch_bounds__(kAttnThreads, 2)
 attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                  const uint16_t* __restrict__ v_cache,
@@ -411,15 +413,15 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // loaded one step before the tile is issued so the scalar load's latency
     // is off the path.
     auto tile_page = [&](int kt) -> int { return pt[(kt * kKeyTile) >> ps_shift]; };
+    bool page_err = false;   // a bad page id on the whole-tile path (recorded once at the end)
     auto issue_tile = [&](int kt, auto stage_c, int page) {
         constexpr int STAGE = decltype(stage_c)::value;
         const int key0 = kt * kKeyTile;
-        if (ps >= kKeyTile) {
+        if (FAST) {
             // one page per tile: uniform base + per-lane constant offsets
-            if (page < 0 || page >= num_pages) {
-                record_error(pv.hdr, b, FB_DERR_PAGE);
-                page = 0;
-            }
+            const bool okp = page >= 0 && page < num_pages;
+            page_err |= !okp;
+            page = okp ? page : 0;
             const size_t inpage = (size_t)(key0 & (ps - 1));
             const uint16_t* kbase = k_cache + (size_t)page * page_elems + k_head + inpage * D;
             const uint16_t* vbase = v_cache + (size_t)page * page_elems + v_head + inpage;
@@ -431,6 +433,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                              :: "s"(m0), "v"(ch_off[j]), "s"(base) : "memory");
             }
         } else {
+            (void)page;
             // several pages per tile: per-lane page selection
             const int pbase = key0 >> ps_shift;
             const int plast = (ke - 1) >> ps_shift;
@@ -630,26 +633,39 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // Stages in use: i (V), i+1 (K), i+2 .. i+NS-1 in flight.
     static_assert(NS >= 3, "the ring needs the current, next and one loading stage");
     floatx16 s_cur = floatx16{};
-    int pg_next = (ps >= kKeyTile && NS - 1 < nt) ? tile_page(kt0 + NS - 1) : 0;
-    auto step = [&](int i, auto stage_c, auto last_c) {
+    int pg_next = (FAST && NS - 1 < nt) ? tile_page(kt0 + NS - 1) : 0;
+    // KIND 0: a step with a refill and the steady-state wait (no runtime
+    // checks); 1: a step near the end; 2: the step that brings in the last
+    // tile (which may be partial).
+    auto step = [&](int i, auto stage_c, auto kind_c) {
         constexpr int STAGE = decltype(stage_c)::value;
-        constexpr bool LAST = decltype(last_c)::value;   // tile i+1 is the last one
+        constexpr int KIND = decltype(kind_c)::value;
         constexpr int NXT = (STAGE + 1) % NS;
         constexpr int FREE = (STAGE + NS - 1) % NS;
-        int behind = nt - 2 - i;            // tiles issued after tile i+1
-        if (behind > NS - 3) behind = NS - 3;
-        wait_vm(behind * NCH);
-        barrier_raw();
-        if (i + NS - 1 < nt) {
+        if constexpr (KIND == 0) {
+            wait_vm((NS - 3) * NCH);
+            barrier_raw();
             issue_tile(kt0 + i + NS - 1, std::integral_constant<int, FREE>{}, pg_next);
-            if (ps >= kKeyTile && i + NS < nt) pg_next = tile_page(kt0 + i + NS);
+            if (FAST) {
+                const int nx = i + NS < nt ? i + NS : nt - 1;   // clamped: no branch
+                pg_next = tile_page(kt0 + nx);
+            }
+        } else {
+            int behind = nt - 2 - i;            // tiles issued after tile i+1
+            if (behind > NS - 3) behind = NS - 3;
+            wait_vm(behind * NCH);
+            barrier_raw();
+            if (i + NS - 1 < nt) {
+                issue_tile(kt0 + i + NS - 1, std::integral_constant<int, FREE>{}, pg_next);
+                if (FAST && i + NS < nt) pg_next = tile_page(kt0 + i + NS);
+            }
         }
         const unsigned char* kst = ring + NXT * RG_::kStageBytes;
         const unsigned char* vst = ring + STAGE * RG_::kStageBytes;   // V^T offsets include the K part
 
         floatx16 s_nxt = floatx16{};
         phase1(kst, s_cur, s_nxt);
-        if constexpr (LAST) {
+        if constexpr (KIND == 2) {
             if (valid_last < kKeyTile) mask_tail(s_nxt);
         }
         const float mx = phase2(vst, s_nxt);
@@ -659,18 +675,25 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 
     if (nt > 0) {
         static_for<NS - 1>([&](auto j) {
-            if (j < nt) issue_tile(kt0 + j, j, ps >= kKeyTile ? tile_page(kt0 + j) : 0);
+            if (j < nt) issue_tile(kt0 + j, j, FAST ? tile_page(kt0 + j) : 0);
         });
         wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
         barrier_raw();
         s_mfmas(ring, s_cur);
         if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
         m_run = tile_max(s_cur);
-        using Mid = std::false_type;
-        using Last = std::true_type;
-        for (int i = 0; i < nt - 2; i += NS) {
+        using Full = std::integral_constant<int, 0>;
+        using Near = std::integral_constant<int, 1>;
+        using Last = std::integral_constant<int, 2>;
+        // steps 0 .. n_full-1 refill the ring (and, as NS >= 3, are not the last)
+        const int n_full = nt - NS + 1 > 0 ? nt - NS + 1 : 0;
+        int i0 = 0;
+        for (; i0 + NS <= n_full; i0 += NS) {
+            static_for<NS>([&](auto j) { step(i0 + j, j, Full{}); });
+        }
+        for (; i0 < nt - 2; i0 += NS) {
             static_for<NS>([&](auto j) {
-                if (i + j < nt - 2) step(i + j, j, Mid{});
+                if (i0 + j < nt - 2) step(i0 + j, j, Near{});
             });
         }
         // the step that brings in the last tile (which may be partial)
@@ -700,6 +723,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         pv_mfmas(slast);
     }
 
+    if (page_err && tid == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
     float l_part = l_acc[0] + l_acc[1];
     const float l = l_part + __shfl_xor(l_part, 32, 64);
     const float inv_l = 1.0f / l;
@@ -983,24 +1007,24 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     const uint16_t* kc = static_cast<const uint16_t*>(k_cache);
     const uint16_t* vc = static_cast<const uint16_t*>(v_cache);
     uint16_t* ob = static_cast<uint16_t*>(out);
+    const bool fast = sh->page_size >= kKeyTile;
+    auto launch = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(z.item_cap), dim3(kAttnThreads), 0, stream, qb, kc, vc,
+                           page_table, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl, z.row_groups,
+                           sh->page_size, shift, sh->max_pages, sh->num_pages, scale_log2);
+    };
     switch (sh->head_dim) {
         case 32:
-            hipLaunchKernelGGL(attn_bf16_kernel<32>, dim3(z.item_cap), dim3(kAttnThreads),
-                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
-                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
-                               sh->max_pages, sh->num_pages, scale_log2);
+            if (fast) launch(attn_bf16_kernel<32, true>);
+            else launch(attn_bf16_kernel<32, false>);
             break;
         case 64:
-            hipLaunchKernelGGL(attn_bf16_kernel<64>, dim3(z.item_cap), dim3(kAttnThreads),
-                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
-                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
-                               sh->max_pages, sh->num_pages, scale_log2);
+            if (fast) launch(attn_bf16_kernel<64, true>);
+            else launch(attn_bf16_kernel<64, false>);
             break;
         default:
-            hipLaunchKernelGGL(attn_bf16_kernel<128>, dim3(z.item_cap), dim3(kAttnThreads),
-                               0, stream, qb, kc, vc, page_table, pv, ws, ob, sh->Hq,
-                               sh->Hkv, g, pack->bl, z.row_groups, sh->page_size, shift,
-                               sh->max_pages, sh->num_pages, scale_log2);
+            if (fast) launch(attn_bf16_kernel<128, true>);
+            else launch(attn_bf16_kernel<128, false>);
             break;
     }
     e = hipGetLastError();
