@@ -266,8 +266,11 @@ __device__ inline void static_for(F&& f) {
 
 template <int D>
 struct Ring {
-    // Stages of the ring: two workgroups per CU share its 160 KB of LDS.
-    static constexpr int kStages = 4;
+    // Stages of the ring: three workgroups per CU (12 waves, 3 per SIMD)
+    // share its 160 KB of LDS -- 3 x 48 KB at D = 128.  The third wave per
+    // SIMD hides more of the exp and DMA issue work behind other waves'
+    // MFMAs than a fourth ring stage would hide load latency.
+    static constexpr int kStages = D == 128 ? 3 : 4;
     static constexpr int kKCh = kKeyTile * D / 8;   // K chunks per stage
     static constexpr int kVCh = D * kKeyTile / 8;   // V^T chunks per stage
     static constexpr int kCh = kKCh + kVCh;
@@ -303,7 +306,7 @@ __device__ inline void wait_vm(int n) {
 // FAST: pages hold whole key tiles (page_size >= 32), so a tile's loads share
 // one scalar base; otherwise each lane picks its page.
 template <int D, bool FAST>
-__global__ void __launch_bounds__(kAttnThreads, 2)
+__global__ void __launch_bounds__(kAttnThreads, 3)
 attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                  const uint16_t* __restrict__ v_cache,
                  const int32_t* __restrict__ page_table, PackView pv, AttnWs ws,
@@ -394,19 +397,18 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // Per-lane LDS byte offsets of the MFMA operand reads (stage 0).
     const int krow = swap_bits23(n);
     const int kswz = krow % CPR;
-    uint32_t koff[KK];
+    // chunk (2kk + h) ^ kswz of row krow: the row part and the chunk part
+    // occupy disjoint bits, so k-step kk is one XOR away from k-step 0
+    const uint32_t kx = (uint32_t)(krow * D + ((h ^ kswz) * 8)) * 2u;
+    auto koff = [&](int kk) -> uint32_t { return kx ^ (uint32_t)(kk << 5); };
+    // V^T rows d = dt*32 + n share the swizzle of row n ((d/4)%4 does not
+    // depend on dt), so d tile dt is a constant offset from d tile 0.
+    uint32_t voff0[2];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-        koff[kk] = (uint32_t)(krow * D + (((kk * 2 + h) ^ kswz) * 8)) * 2u;
-    uint32_t voff[DT][2];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const int d = dt * 32 + n;
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-            voff[dt][tt] = RG_::kKCh * 16 +
-                           (uint32_t)(d * kKeyTile + (((tt * 2 + h) ^ ((d >> 2) & 3)) * 8)) * 2u;
-    }
+    for (int tt = 0; tt < 2; ++tt)
+        voff0[tt] = RG_::kKCh * 16 + (uint32_t)(n * kKeyTile + (((tt * 2 + h) ^ ((n >> 2) & 3)) * 8)) * 2u;
+    constexpr uint32_t kVdt = 32 * kKeyTile * 2;   // bytes between d tiles of V^T
+    auto voff = [&](int dt, int tt) -> uint32_t { return voff0[tt] + dt * kVdt; };
 
     // Issue the loads of key tile kt into stage STAGE.
     // Page id of key tile kt when a page holds whole tiles (ps >= kKeyTile);
@@ -479,36 +481,36 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const int kt0 = kb / kKeyTile;
     const int nt = (ke + kKeyTile - 1) / kKeyTile - kt0;
     const int valid_last = ke - (kt0 + nt - 1) * kKeyTile;   // keys of the last tile below ke
-    constexpr int kAhead = KK < 4 ? KK : 4;   // LDS operand reads kept in flight
+    constexpr int kAhead = KK < 2 ? KK : 2;   // LDS operand reads kept in flight
 
     // S^T of one key tile (K fragments from stage kst) into acc.
     auto s_mfmas = [&](const unsigned char* kst, floatx16& acc) {
         bf16x8 fr[kAhead];
 #pragma unroll
-        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff[m]);
+        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff(m));
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8 a = fr[kk % kAhead];
             if (kk + kAhead < KK)
-                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff[kk + kAhead]);
+                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff(kk + kAhead));
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
         }
     };
     // O^T += V^T P^T of one key tile (V^T fragments from stage vst).
     auto pv_mfmas = [&](const unsigned char* vst) {
         constexpr int NX = DT * 2;
-        constexpr int A = NX < 4 ? NX : 4;
+        constexpr int A = NX < 2 ? NX : 2;
         bf16x8 fr[A];
         // product x: d tile x % DT, key half x / DT (consecutive products
         // accumulate into different tiles)
 #pragma unroll
         for (int x = 0; x < A; ++x)
-            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x % DT][x / DT]);
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff(x % DT, x / DT));
 #pragma unroll
         for (int x = 0; x < NX; ++x) {
             const bf16x8 a = fr[x % A];
             if (x + A < NX)
-                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) % DT][(x + A) / DT]);
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff((x + A) % DT, (x + A) / DT));
             o[x % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x / DT], o[x % DT], 0, 0, 0);
         }
     };
@@ -574,13 +576,13 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
         bf16x8 fr[kAhead];
 #pragma unroll
-        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff[m]);
+        for (int m = 0; m < kAhead; ++m) fr[m] = *reinterpret_cast<const bf16x8*>(kst + koff(m));
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8 a = fr[kk % kAhead];
             if (kk + kAhead < KK)
-                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff[kk + kAhead]);
+                fr[kk % kAhead] = *reinterpret_cast<const bf16x8*>(kst + koff(kk + kAhead));
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
 #pragma unroll
             for (int y = 0; y < SPG; y += 2) {
@@ -599,19 +601,19 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // while the VALU takes the row max of the next tile's scores.
     auto phase2 = [&](const unsigned char* vst, const floatx16& sn) -> float {
         constexpr int NX = DT * 2;
-        constexpr int A = NX < 4 ? NX : 4;
+        constexpr int A = NX < 2 ? NX : 2;
         constexpr int VPG = 16 / NX;   // scores per group
         bf16x8 fr[A];
 #pragma unroll
         for (int x = 0; x < A; ++x)
-            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff[x % DT][x / DT]);
+            fr[x] = *reinterpret_cast<const bf16x8*>(vst + voff(x % DT, x / DT));
         float mx = -INFINITY;
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int x = 0; x < NX; ++x) {
             const bf16x8 a = fr[x % A];
             if (x + A < NX)
-                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff[(x + A) % DT][(x + A) / DT]);
+                fr[x % A] = *reinterpret_cast<const bf16x8*>(vst + voff((x + A) % DT, (x + A) / DT));
             o[x % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[x / DT], o[x % DT], 0, 0, 0);
 #pragma unroll
             for (int y = 0; y < VPG; ++y) mx = fmaxf(mx, sn[x * VPG + y]);
@@ -709,13 +711,24 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         unsigned char* slast = ring + last_stage * RG_::kStageBytes;
         if (valid_last < kKeyTile) {
             // V^T columns of keys past ke may hold anything (even NaN); zero
-            // them so their 0-weight products stay 0.
-            uint16_t* vlds = reinterpret_cast<uint16_t*>(slast + RG_::kKCh * 16);
-            for (int e = tid; e < D * kKeyTile; e += kAttnThreads) {
-                const int d = e / kKeyTile, key = e % kKeyTile;
-                if (key >= valid_last) {
-                    const int pos = (key >> 3) ^ ((d >> 2) & 3);
-                    vlds[d * kKeyTile + pos * 8 + (key & 7)] = 0;
+            // them so their 0-weight products stay 0.  One 16-byte chunk (8
+            // keys of one d) per thread and pass.
+            unsigned char* vlds = slast + RG_::kKCh * 16;
+#pragma unroll 1
+            for (int e = tid; e < D * (kKeyTile / 8); e += kAttnThreads) {
+                const int d = e >> 2, kc = e & 3;
+                const int first = valid_last - kc * 8;   // keys >= first are past ke
+                if (first >= 8) continue;
+                uint4* p = reinterpret_cast<uint4*>(vlds + (d * kKeyTile + ((kc ^ ((d >> 2) & 3)) * 8)) * 2);
+                if (first <= 0) {
+                    *p = make_uint4(0, 0, 0, 0);
+                } else {
+                    const uint4 v = *p;
+                    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        if (k >= first) w[k >> 1] &= (k & 1) ? 0x0000ffffu : 0xffff0000u;
+                    *p = make_uint4(w[0], w[1], w[2], w[3]);
                 }
             }
             barrier_raw();

@@ -65,6 +65,9 @@ def test_serve256_sampled_requests():
     dict(d=64, Hq=8, Hkv=8),                        # no GQA
     dict(d=32, Hq=16, Hkv=2),                       # group of 8
     dict(bl=16, page_size=16, W_max=5, window=("fixed", 5)),
+    dict(bl=64, page_size=64, W_max=4, window=("uniform", 1, 4)),   # Table 2 lengths
+    dict(bl=96, page_size=32, W_max=3, window=("fixed", 3)),        # bl not a power of 2
+    dict(bl=128, page_size=128, W_max=5, window=("fixed", 5), prefix_jitter=40),
     dict(V=1001, prefix_jitter=5),                  # unaligned logit rows
     dict(B=5, layout="padded", window=("uniform", 1, 3)),
 ])
