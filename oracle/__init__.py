@@ -23,7 +23,13 @@ reordering beyond what the definition states:
                     Sec. 3.1 post-edit steps, Alg. 1 retire / gated admit, Eq. 3.
 * ``serial``     -- an independently written serial block-wise decoder (one
                     block at a time), the W = 1 special case of Alg. 1.
-* ``step``       -- one whole wavefront step = pack, KV write, attention, update.
+* ``step``       -- one whole wavefront step = pack, KV write, attention, update;
+                    the multi-step loop of Alg. 1, per-request windows (HWP) or
+                    one shared window (the synchronous variant of the Sec. 5
+                    ablation).
+* ``synth_model`` -- a deterministic SplitMix64 hash model standing in for
+                    f_theta in the loop (no weights exist here), with the
+                    block-causal visibility of Sec. 4.1.
 
 Readings of points the paper leaves open (all shared with the HIP path by
 specification, never by code) are listed in ``READINGS`` below.
@@ -48,4 +54,4 @@ READINGS = {
     "scale": "Softmax scale 1/sqrt(d); query head h reads kv-head h // (Hq/Hkv).",
 }
 
-from . import pack, attention, bruteforce, update, serial, step  # noqa: E402,F401
+from . import pack, attention, bruteforce, update, serial, step, synth_model  # noqa: E402,F401

@@ -53,8 +53,8 @@ def serial_decode(model, x, prompt_len, gen_start, n, bl, params,
                   max_forwards=10_000):
     """Decode one sequence block by block.
 
-    model(x, lo, hi) -> float64 logits [hi - lo, V] for positions [lo, hi)
-    given the context x[:hi].  Each block is refined by the joint M2T/T2T rule
+    model(x, lo, hi, gen_start=...) -> float64 logits [hi - lo, V] for
+    positions [lo, hi) given the context x[:hi].  Each block is refined by the joint M2T/T2T rule
     (Eq. 1) until it is locally finished (Sec. 3.1): once it has no masks, up
     to S_pe post-edit steps, stopping early after a step with no change.  The
     block then commits; a committed eos_id ends decoding.
@@ -70,7 +70,7 @@ def serial_decode(model, x, prompt_len, gen_start, n, bl, params,
         lo = gen_start + g * bl
         post_edits = 0
         while True:
-            z = model(x, lo, lo + bl)
+            z = model(x, lo, lo + bl, gen_start=gen_start)
             forwards += 1
             if forwards > max_forwards:
                 raise RuntimeError("serial decoder did not converge")

@@ -53,7 +53,9 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
     tokens    : int64 [B, T_max]; not modified (a copy is returned)
     state     : dict of per-request int arrays; pe, fin: int [B, n_max]
     params    : dict tau_mask, tau_edit, theta, mask_id, eos_id, S_pe, W,
-                edit_masked (bool), force_progress (bool)
+                edit_masked (bool), force_progress (bool), sync_window (bool:
+                one window shared by the batch, the synchronous variant that
+                the Sec. 5 ablation compares HWP with)
     returns dict: tokens, conf (float32 per row, 0 for dead rows),
                   argmax (per row, -1 for dead rows), state, pe, fin,
                   stats (per request), band_rows, band_reqs
@@ -81,6 +83,7 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
     for t in packed["tiles"]:
         tiles_of[t["b"]].append(t)
 
+    rho_of = [None] * B
     for b in range(B):
         tl = tiles_of[b]
         rho = {}
@@ -139,48 +142,117 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
                 fin[b, g] = 1
         if tl:
             stats[b]["rho"] = rho[tl[-1]["g"]]
-        if not st["active"][b]:
-            continue
-        n = int(st["n_blocks"][b])
-        # --- in-order retirement (Alg. 1 inner while; Sec. 4.1 last para) ---
-        while st["L"][b] < st["R"][b] and fin[b, st["L"][b]]:
-            g = int(st["L"][b])
-            st["L"][b] += 1
-            stats[b]["committed"] += 1
-            if eos_id >= 0:
-                lo = int(st["gen_start"][b]) + g * bl
-                if np.any(tokens[b, lo:lo + bl] == eos_id):
-                    st["active"][b] = 0
-                    st["eos_hit"][b] = 1
-                    stats[b]["eos"] = 1
-                    stats[b]["done"] = 1
-                    break
-        if st["active"][b] and st["L"][b] >= n:
-            st["active"][b] = 0
-            stats[b]["done"] = 1
-        if not st["active"][b]:
-            continue
-        # --- gated admission (Eq. 3; Alg. 1 second inner while) ---
-        if st["L"][b] == st["R"][b] and st["R"][b] < n:
-            g = int(st["R"][b])
-            st["R"][b] += 1
-            pe[b, g] = 0
-            fin[b, g] = 0
-            rho[g] = 0.0
-            stats[b]["spawned"] += 1
-        while (st["R"][b] - st["L"][b] < W and st["R"][b] < n
-               and _rho_of(rho, int(st["R"][b]) - 1, int(st["L"][b])) >= theta):
-            g = int(st["R"][b])
-            st["R"][b] += 1
-            pe[b, g] = 0
-            fin[b, g] = 0
-            rho[g] = 0.0
-            stats[b]["spawned"] += 1
+        rho_of[b] = rho
+
+    if params.get("sync_window", False):
+        _sync_retire_admit(tokens, st, pe, fin, rho_of, stats, bl, params)
+    else:
+        for b in range(B):
+            _retire_admit(b, tokens, st, pe, fin, rho_of[b], stats, bl, params)
 
     band_reqs = sorted({int(packed["row_req"][r]) for r in band_rows})
     return dict(tokens=tokens, conf=conf, argmax=argmax, state=st, pe=pe,
                 fin=fin, stats=stats, band_rows=sorted(band_rows),
                 band_reqs=band_reqs)
+
+
+def _retire_admit(b, tokens, st, pe, fin, rho, stats, bl, params):
+    """Alg. 1's two inner loops for request b alone (HWP, Sec. 4.2: every
+    request keeps its own window)."""
+    eos_id, W, theta = params["eos_id"], params["W"], params["theta"]
+    if not st["active"][b]:
+        return
+    n = int(st["n_blocks"][b])
+    # --- in-order retirement (Alg. 1 inner while; Sec. 4.1 last para) ---
+    while st["L"][b] < st["R"][b] and fin[b, st["L"][b]]:
+        g = int(st["L"][b])
+        st["L"][b] += 1
+        stats[b]["committed"] += 1
+        if eos_id >= 0:
+            lo = int(st["gen_start"][b]) + g * bl
+            if np.any(tokens[b, lo:lo + bl] == eos_id):
+                st["active"][b] = 0
+                st["eos_hit"][b] = 1
+                stats[b]["eos"] = 1
+                stats[b]["done"] = 1
+                break
+    if st["active"][b] and st["L"][b] >= n:
+        st["active"][b] = 0
+        stats[b]["done"] = 1
+    if not st["active"][b]:
+        return
+    # --- gated admission (Eq. 3; Alg. 1 second inner while) ---
+    if st["L"][b] == st["R"][b] and st["R"][b] < n:
+        g = int(st["R"][b])
+        st["R"][b] += 1
+        pe[b, g] = 0
+        fin[b, g] = 0
+        rho[g] = 0.0
+        stats[b]["spawned"] += 1
+    while (st["R"][b] - st["L"][b] < W and st["R"][b] < n
+           and _rho_of(rho, int(st["R"][b]) - 1, int(st["L"][b])) >= theta):
+        g = int(st["R"][b])
+        st["R"][b] += 1
+        pe[b, g] = 0
+        fin[b, g] = 0
+        rho[g] = 0.0
+        stats[b]["spawned"] += 1
+
+
+def _sync_retire_admit(tokens, st, pe, fin, rho_of, stats, bl, params):
+    """The batch-synchronous wavefront that the ablation of Sec. 5 compares
+    HWP against (and Sec. 4.2 describes): all active requests share one window
+    [L, R); block L retires only when it is finished in every active request
+    (finished.all()), and the gate of Eq. 3 uses the smallest rho over the
+    active requests.  A request whose committed block holds eos_id stops; the
+    others go on.  With one request this is exactly ``_retire_admit``."""
+    eos_id, W, theta = params["eos_id"], params["W"], params["theta"]
+    act = [b for b in range(len(st["L"])) if st["active"][b]]
+    if not act:
+        return
+    L, R, n = (int(st[k][act[0]]) for k in ("L", "R", "n_blocks"))
+    for b in act:
+        if (int(st["L"][b]), int(st["R"][b]), int(st["n_blocks"][b])) != (L, R, n):
+            raise ValueError("a synchronous wavefront needs one shared window")
+    # --- retirement: the shared block L goes when every active request finished it
+    while L < R and act and all(fin[b, L] for b in act):
+        g = L
+        L += 1
+        still = []
+        for b in act:
+            st["L"][b] = L
+            stats[b]["committed"] += 1
+            lo = int(st["gen_start"][b]) + g * bl
+            if eos_id >= 0 and np.any(tokens[b, lo:lo + bl] == eos_id):
+                st["active"][b] = 0
+                st["eos_hit"][b] = 1
+                stats[b]["eos"] = 1
+                stats[b]["done"] = 1
+            else:
+                still.append(b)
+        act = still
+    if L >= n:
+        for b in act:
+            st["active"][b] = 0
+            stats[b]["done"] = 1
+        act = []
+    if not act:
+        return
+    # --- admission gated by the minimum readiness over the batch (Eq. 3)
+    def admit(R):
+        for b in act:
+            pe[b, R] = 0
+            fin[b, R] = 0
+            rho_of[b][R] = 0.0
+            stats[b]["spawned"] += 1
+        return R + 1
+    if L == R and R < n:
+        R = admit(R)
+    while (R - L < W and R < n
+           and min(_rho_of(rho_of[b], R - 1, L) for b in act) >= theta):
+        R = admit(R)
+    for b in act:
+        st["R"][b] = R
 
 
 def _rho_of(rho, g, L):

@@ -36,6 +36,20 @@ MUTATIONS = [
      "softmax scale"),
     ("attention.py", "S = S - S.max(axis=1, keepdims=True)\n    P = np.exp(S)\n    P = P / P.sum(axis=1, keepdims=True)",
      "P = np.exp(S)", "softmax not normalised"),
+    ("update.py", "all(fin[b, L] for b in act)", "any(fin[b, L] for b in act)",
+     "synchronous retire on any() instead of all()"),
+    ("update.py", "min(_rho_of(rho_of[b], R - 1, L) for b in act)",
+     "max(_rho_of(rho_of[b], R - 1, L) for b in act)",
+     "synchronous gate on the largest readiness"),
+    ("synth_model.py", "z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64",
+     "z = ((z ^ (z >> 26)) * 0x94D049BB133111EB) & MASK64", "hash mix shift"),
+    ("synth_model.py", "    for j in range(hi):\n", "    for j in range(lo):\n",
+     "model context misses the block's own tokens"),
+    ("synth_model.py", "for j in range(gen_start, lo) if int(x[j]) == mask_id)",
+     "for j in range(gen_start, hi) if int(x[j]) == mask_id)",
+     "staleness counts the block's own masks"),
+    ("synth_model.py", "lvl = 3 if p == first else (h >> 32) % 4",
+     "lvl = (h >> 32) % 4", "no guaranteed reveal per forward"),
 ]
 
 
@@ -45,7 +59,8 @@ def _plant(tmp, fname, old, new):
                     ignore=shutil.ignore_patterns("__pycache__"))
     tdst = os.path.join(tmp, "tests")
     os.makedirs(tdst)
-    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_traces.py"):
+    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_traces.py",
+              "test_oracle_loop.py"):
         shutil.copy(os.path.join(ROOT, "tests", f), tdst)
     shutil.copytree(os.path.join(ROOT, "tests", "golden"),
                     os.path.join(tdst, "golden"))
@@ -63,7 +78,8 @@ def test_pins_catch_planted_mistake(tmp_path, fname, old, new, what):
     env = dict(os.environ, PYTHONDONTWRITEBYTECODE="1")
     proc = subprocess.run(
         [sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-         "tests/test_oracle_pins.py", "tests/test_oracle_traces.py"],
+         "tests/test_oracle_pins.py", "tests/test_oracle_traces.py",
+         "tests/test_oracle_loop.py"],
         cwd=str(tmp_path), env=env, capture_output=True, text=True, timeout=300)
     assert proc.returncode != 0, f"pins did not catch: {what}\n{proc.stdout[-2000:]}"
     assert "failed" in proc.stdout or "error" in proc.stdout.lower()

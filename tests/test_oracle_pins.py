@@ -265,7 +265,7 @@ def toy_model(V, bl_salt=0):
     and the predicted id depends on the visible tokens, so drafts get edited
     as context fills in.  The first masked position of a block is always
     confident, so every forward reveals at least one token."""
-    def model(x, lo, hi):
+    def model(x, lo, hi, gen_start=0):
         M = V - 1
         vis = x[:hi]
         revealed = int(np.sum(vis != M))
@@ -298,12 +298,12 @@ def test_gwd_with_window_one_equals_serial_decoding(S_pe):
     state = dict(gen_start=np.array([prompt]), prompt_len=np.array([prompt]),
                  n_blocks=np.array([n]), L=np.array([0]), R=np.array([1]),
                  active=np.array([1]), eos_hit=np.array([0]))
-    toks, st, steps, forwards = step.gwd_loop(
+    res = step.gwd_loop(
         model, state, x0[None, :], np.zeros((1, n), dtype=np.int64),
         np.zeros((1, n), dtype=np.int64), prm, 1, bl, pack.RAGGED)
-    assert np.array_equal(toks[0], ser)
-    assert forwards[0] == fwd
-    assert committed == n and st["L"][0] == n
+    assert np.array_equal(res["tokens"][0], ser)
+    assert res["forwards"][0] == fwd
+    assert committed == n and res["state"]["L"][0] == n
 
 
 def test_gwd_batch_equals_each_request_alone():
@@ -325,14 +325,13 @@ def test_gwd_batch_equals_each_request_alone():
                  eos_hit=np.zeros(B, dtype=np.int64))
     z = np.zeros((B, n), dtype=np.int64)
     model = toy_model(V)
-    toks, st, _, fw = step.gwd_loop(model, state, x0, z, z, prm, 2, bl,
-                                    pack.PADDED)
+    res = step.gwd_loop(model, state, x0, z, z, prm, 2, bl, pack.PADDED)
     for b in range(B):
         s1 = {k: v[b:b + 1].copy() for k, v in state.items()}
-        t1, _, _, f1 = step.gwd_loop(model, s1, x0[b:b + 1], z[:1], z[:1], prm,
-                                     2, bl, pack.RAGGED)
-        assert np.array_equal(t1[0], toks[b])
-        assert f1[0] == fw[b]
+        r1 = step.gwd_loop(model, s1, x0[b:b + 1], z[:1], z[:1], prm, 2, bl,
+                           pack.RAGGED)
+        assert np.array_equal(r1["tokens"][0], res["tokens"][b])
+        assert r1["forwards"][0] == res["forwards"][b]
 
 
 def test_wavefront_is_no_slower_than_serial_in_forwards():
@@ -351,7 +350,6 @@ def test_wavefront_is_no_slower_than_serial_in_forwards():
                  n_blocks=np.array([n]), L=np.array([0]), R=np.array([1]),
                  active=np.array([1]), eos_hit=np.array([0]))
     z = np.zeros((1, n), dtype=np.int64)
-    _, st, steps, fw = step.gwd_loop(model, state, x0[None], z, z, prm, 2, bl,
-                                     pack.RAGGED)
-    assert st["L"][0] == n
-    assert fw[0] <= fwd_serial
+    res = step.gwd_loop(model, state, x0[None], z, z, prm, 2, bl, pack.RAGGED)
+    assert res["state"]["L"][0] == n
+    assert res["forwards"][0] <= fwd_serial
