@@ -80,6 +80,12 @@ extern "C" {
 #define FB_EDIT_MASKED    1u  /* literal Eq. 1: T2T may also overwrite [M]     */
 #define FB_FORCE_PROGRESS 2u  /* a block with masks but no M2T this step
                                  unmasks its most confident masked row         */
+#define FB_SYNC_WINDOW    4u  /* the batch-synchronous wavefront that the
+                                 Sec. 5 ablation compares HWP with: every
+                                 active request shares one window [L, R);
+                                 block L retires only when it is finished in
+                                 all of them and admission (Eq. 3) gates on the
+                                 smallest rho over them                        */
 
 /* Per-request wavefront state (Sec. 4.2: "independent wavefront states
  * (L_b, R_b), finished flags, and in-order commit pointer").  Device array
@@ -149,7 +155,8 @@ typedef struct fb_update_params {
     int32_t  eos_id;       /* < 0 disables the EOS stop                        */
     int32_t  S_pe;         /* post-edit step cap (Sec. 3.1)                    */
     int32_t  W;            /* admission cap, 1 <= W <= W_max of the pack       */
-    uint32_t flags;        /* FB_EDIT_MASKED | FB_FORCE_PROGRESS               */
+    uint32_t flags;        /* FB_EDIT_MASKED | FB_FORCE_PROGRESS |
+                              FB_SYNC_WINDOW                                   */
     int32_t  reserved[3];
 } fb_update_params;
 
@@ -273,6 +280,11 @@ size_t fb_update_workspace_bytes(const fb_pack* pack, int V);
  *  5. admit (Eq. 3): if the window is empty admit one block; then while
  *     R - L < W, R < n and rho(B_{R-1}) >= theta_spawn: R++ (a block admitted
  *     in this step has rho = 0).
+ *  With FB_SYNC_WINDOW, steps 4 and 5 act on the window all active requests
+ *  share: retire while every one of them has finished B_L (a committed eos_id
+ *  still stops only its own request), admit while the minimum of rho(B_{R-1})
+ *  over them passes theta_spawn.  Active requests whose (L, R, n) differ are
+ *  recorded as FB_DERR_STATE and no request retires or admits in that call.
  *   logits  [row_cap][V], dtype FB_BF16 or FB_F32; rows not live are not read
  *   tokens  int32[B][T_max], updated in place
  *   conf, argmax  [row_cap]; only live rows are written

@@ -53,7 +53,8 @@ def gwd_loop(model, state, tokens, pe, fin, params, W_max, bl, layout,
     q/k/v rows (``synth_model.embed_rows`` of each live row's position and its
     token at the start of the step); K, V are the logical per-request caches
     (float64 [T, Hkv, d]), updated in place.  The attention output of the last
-    step is returned under "out" as {(b, pos): [Hq, d]}.
+    step is returned under "out_last" as {(b, pos): [Hq, d]}, that step's
+    packed rows under "packed_last".
 
     Returns dict(tokens, state, pe, fin, steps, forwards) (+ out, K, V)."""
     from . import synth_model
@@ -64,7 +65,7 @@ def gwd_loop(model, state, tokens, pe, fin, params, W_max, bl, layout,
     B = len(state["L"])
     forwards = np.zeros(B, dtype=np.int64)
     steps = 0
-    last_out = {}
+    last_out, last_packed = {}, None
     while np.any(state["active"]):
         steps += 1
         if steps > max_steps:
@@ -86,6 +87,7 @@ def gwd_loop(model, state, tokens, pe, fin, params, W_max, bl, layout,
                                              kv["Hq"], kv["Hkv"])
             last_out = {(int(packed["row_req"][r]), int(packed["row_pos"][r])): out[r]
                         for r in live}
+            last_packed = packed
         xhat = np.full(packed["cap"], -1, dtype=np.int64)
         p64 = np.zeros(packed["cap"])
         for t in packed["tiles"]:
@@ -103,5 +105,5 @@ def gwd_loop(model, state, tokens, pe, fin, params, W_max, bl, layout,
     out = dict(tokens=tokens, state=state, pe=pe, fin=fin, steps=steps,
                forwards=forwards)
     if kv is not None:
-        out.update(out_last=last_out, K=kv["K"], V=kv["V"])
+        out.update(out_last=last_out, packed_last=last_packed, K=kv["K"], V=kv["V"])
     return out

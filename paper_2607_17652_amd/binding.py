@@ -30,16 +30,18 @@ FB_RAGGED = 0
 FB_PADDED = 1
 FB_EDIT_MASKED = 1
 FB_FORCE_PROGRESS = 2
+FB_SYNC_WINDOW = 4
 
 LAYOUTS = {"ragged": FB_RAGGED, "padded": FB_PADDED}
 
-# Every symbol include/flowblock.h declares.
+# Every symbol include/*.h declares.
 EXPORTS = [
     "fb_version", "fb_last_error", "fb_pack_bytes", "fb_pack_get_offsets",
     "fb_pack_init", "fb_pack_wavefronts", "fb_pack_read_status",
     "fb_write_window_kv", "fb_attention_workspace_bytes",
     "fb_wavefront_attention", "fb_update_workspace_bytes", "fb_denoise_update",
     "fb_vocab_reduce", "fb_denoise_apply",
+    "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
 ]
 
 
@@ -76,6 +78,25 @@ class fb_update_params(ctypes.Structure):
                 ("eos_id", ctypes.c_int32), ("S_pe", ctypes.c_int32),
                 ("W", ctypes.c_int32), ("flags", ctypes.c_uint32),
                 ("reserved", ctypes.c_int32 * 3)]
+
+
+class fb_synth_model(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("levels", ctypes.c_float * 4)]
+
+
+class fb_loop_args(ctypes.Structure):
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    _fields_ = [
+        ("st", vp), ("tokens", vp), ("T_max", i32), ("n_max", i32), ("pe", vp),
+        ("fin", vp), ("pack", ctypes.POINTER(fb_pack)),
+        ("prm", ctypes.POINTER(fb_update_params)),
+        ("model", ctypes.POINTER(fb_synth_model)), ("logits", vp), ("V", i32),
+        ("logit_dtype", i32), ("pred", vp), ("conf", vp), ("argmax", vp),
+        ("stats", vp), ("upd_ws", vp), ("upd_ws_bytes", sz),
+        ("shape", ctypes.POINTER(fb_attn_shape)), ("q", vp), ("k_new", vp),
+        ("v_new", vp), ("k_cache", vp), ("v_cache", vp), ("page_table", vp),
+        ("attn_out", vp), ("attn_ws", vp), ("attn_ws_bytes", sz),
+        ("embed_seed", ctypes.c_uint64), ("counters", vp), ("forwards", vp)]
 
 
 # numpy views of the device records
@@ -123,6 +144,12 @@ def lib():
             "fb_denoise_apply": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, i32,
                                        P(fb_pack), P(fb_update_params), vp, vp, sz,
                                        vp]),
+            "fb_synth_embed": (i32, [P(fb_pack), P(fb_attn_shape), ctypes.c_uint64,
+                                     vp, vp, vp, vp]),
+            "fb_synth_logits": (i32, [vp, vp, i32, P(fb_pack), P(fb_synth_model),
+                                      i32, i32, vp, vp, vp]),
+            "fb_decode_loop": (i32, [P(fb_loop_args), i32, i32, i32, P(i32), P(i32),
+                                     vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -270,9 +297,10 @@ def fb_wavefront_attention(q, k_cache, v_cache, page_table, pack, shape, out,
 
 # ------------------------------------------------------------------- update
 def make_params(tau_mask, tau_edit, theta, mask_id, eos_id, S_pe, W,
-                edit_masked=False, force_progress=False):
+                edit_masked=False, force_progress=False, sync_window=False):
     flags = (FB_EDIT_MASKED if edit_masked else 0) | \
-        (FB_FORCE_PROGRESS if force_progress else 0)
+        (FB_FORCE_PROGRESS if force_progress else 0) | \
+        (FB_SYNC_WINDOW if sync_window else 0)
     return fb_update_params(tau_mask, tau_edit, theta, mask_id, eos_id, S_pe, W,
                             flags)
 
@@ -314,3 +342,36 @@ def fb_denoise_apply(V, tokens, conf, argmax, st, pe, fin, pack, params, stats, 
 def stats_to_numpy(stats_tensor, B):
     raw = stats_tensor.cpu().numpy().view(np.uint8)[: B * REQ_STATS_DTYPE.itemsize]
     return raw.view(REQ_STATS_DTYPE)
+
+
+# ------------------------------------------------------ multi-step loop
+def make_model(seed, levels):
+    m = fb_synth_model()
+    m.seed = seed
+    for i, a in enumerate(levels):
+        m.levels[i] = a
+    return m
+
+
+def fb_synth_embed(pack, shape, seed, q, k_new, v_new, stream=None):
+    _check(lib().fb_synth_embed(pack.ref(), ctypes.byref(shape), seed, _ptr(q),
+                                _ptr(k_new), _ptr(v_new), _stream(stream)))
+
+
+def fb_synth_logits(st, tokens, pack, model, pred, logits, stream=None):
+    """st int32 [B, 8]; tokens int32 [B, T_max]; pred int32 [row_cap, 2];
+    logits [row_cap, V] (bf16 or fp32)."""
+    _check(lib().fb_synth_logits(_ptr(st), _ptr(tokens), tokens.shape[-1],
+                                 pack.ref(), ctypes.byref(model), logits.shape[-1],
+                                 _dtype_code(logits), _ptr(pred), _ptr(logits),
+                                 _stream(stream)))
+
+
+def fb_decode_loop(args, max_steps, check_every, use_graph, stream=None):
+    """args: an fb_loop_args (its pointer fields must stay alive for the call).
+    Returns (steps enqueued, done)."""
+    steps, done = ctypes.c_int(), ctypes.c_int()
+    _check(lib().fb_decode_loop(ctypes.byref(args), max_steps, check_every,
+                                1 if use_graph else 0, ctypes.byref(steps),
+                                ctypes.byref(done), _stream(stream)))
+    return steps.value, bool(done.value)

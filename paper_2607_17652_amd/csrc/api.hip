@@ -237,7 +237,7 @@ int check_update_args(const fb_pack* pack, int V, const void* tokens, const void
         return fail(FB_E_INVAL, "mask_id %d outside [0, V)", prm->mask_id);
     if (isnan(prm->tau_mask) || isnan(prm->tau_edit) || isnan(prm->theta_spawn))
         return fail(FB_E_INVAL, "a threshold is NaN");
-    if (prm->flags & ~(FB_EDIT_MASKED | FB_FORCE_PROGRESS))
+    if (prm->flags & ~(FB_EDIT_MASKED | FB_FORCE_PROGRESS | FB_SYNC_WINDOW))
         return fail(FB_E_INVAL, "unknown flag bits 0x%x", prm->flags);
     return FB_OK;
 }
@@ -314,6 +314,224 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int
     e = fb::launch_apply(tokens, T_max, conf, argmax, st, pe, fin, n_max, pack, prm, stats,
                          ws, z, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "update launch");
+    return ok();
+}
+
+// ---- multi-step loop on the synthetic model (flowblock_loop.h) -----------
+
+namespace {
+
+bool exact_in(float a, int dtype) {
+    if (dtype == FB_F32) return true;
+    uint32_t u;
+    memcpy(&u, &a, 4);
+    return (u & 0xffffu) == 0;   // a bf16 value: the low half of the float is zero
+}
+
+int check_model(const fb_synth_model* m, int V, int dtype) {
+    if (!m) return fail(FB_E_INVAL, "model is NULL");
+    if (V < 2) return fail(FB_E_INVAL, "the synthetic model needs V >= 2");
+    if (dtype != FB_BF16 && dtype != FB_F32)
+        return fail(FB_E_UNSUPPORTED, "logit dtype %d not supported", dtype);
+    for (int l = 0; l < 4; ++l) {
+        const float a = m->levels[l];
+        if (!(a > 0.0f) || isinf(a))
+            return fail(FB_E_INVAL, "level %d (%g) must be finite and > 0", l, (double)a);
+        if (!exact_in(a, dtype))
+            return fail(FB_E_INVAL, "level %d (%g) is not exact in bf16", l, (double)a);
+    }
+    return FB_OK;
+}
+
+int check_embed_args(const fb_pack* pack, const fb_attn_shape* sh, const void* q,
+                     const void* k_new, const void* v_new) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_shape(pack, sh);
+    if (rc) return rc;
+    if (!q || !k_new || !v_new) return fail(FB_E_INVAL, "q, k_new or v_new is NULL");
+    return FB_OK;
+}
+
+int check_logit_args(const fb_req_state* st, const int32_t* tokens, int T_max,
+                     const fb_pack* pack, const fb_synth_model* m, int V, int dtype,
+                     const int32_t* pred, const void* logits) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_model(m, V, dtype);
+    if (rc) return rc;
+    if (!st || !tokens || !pred || !logits) return fail(FB_E_INVAL, "a pointer is NULL");
+    if (T_max < 1) return fail(FB_E_INVAL, "T_max must be >= 1");
+    if (((uintptr_t)pred & 7u) != 0) return fail(FB_E_INVAL, "pred must be 8-byte aligned");
+    if (!aligned16(logits)) return fail(FB_E_INVAL, "logits must be 16-byte aligned");
+    return FB_OK;
+}
+
+// Enqueue one step of the loop (validated by the caller).
+hipError_t enqueue_step(const fb_loop_args* a, const fb::AttnPlanSizes* az,
+                        const fb::UpdateSizes& uz, hipStream_t s) {
+    hipError_t e = fb::launch_loop_count(a->st, a->pack->B, a->counters, a->forwards, 1, s);
+    if (e != hipSuccess) return e;
+    e = fb::launch_pack(a->st, a->tokens, a->n_max, a->T_max, a->pack, s);
+    if (e != hipSuccess) return e;
+    if (a->shape) {
+        e = fb::launch_synth_embed(a->pack, a->shape, a->embed_seed, a->q, a->k_new, a->v_new,
+                                   s);
+        if (e != hipSuccess) return e;
+        e = fb::launch_write_kv(a->k_new, a->v_new, a->k_cache, a->v_cache, a->page_table,
+                                a->pack, a->shape, s);
+        if (e != hipSuccess) return e;
+        e = fb::launch_attention(a->q, a->k_cache, a->v_cache, a->page_table, a->pack,
+                                 a->shape, a->attn_out, a->attn_ws, *az, s);
+        if (e != hipSuccess) return e;
+    }
+    e = fb::launch_synth_logits(a->st, a->tokens, a->T_max, a->pack, a->model, a->V,
+                                a->logit_dtype, a->pred, a->logits, s);
+    if (e != hipSuccess) return e;
+    e = fb::launch_vocab_reduce(a->logits, a->V, a->logit_dtype, a->pack, a->upd_ws, uz, s);
+    if (e != hipSuccess) return e;
+    return fb::launch_apply(a->tokens, a->T_max, a->conf, a->argmax, a->st, a->pe, a->fin,
+                            a->n_max, a->pack, a->prm, a->stats, a->upd_ws, uz, s);
+}
+
+}  // namespace
+
+int fb_synth_embed(const fb_pack* pack, const fb_attn_shape* sh, uint64_t seed, void* q,
+                   void* k_new, void* v_new, void* stream) {
+    int rc = check_embed_args(pack, sh, q, k_new, v_new);
+    if (rc) return rc;
+    hipError_t e = fb::launch_synth_embed(pack, sh, seed, q, k_new, v_new, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "synthetic embedding launch");
+    return ok();
+}
+
+int fb_synth_logits(const fb_req_state* st, const int32_t* tokens, int T_max,
+                    const fb_pack* pack, const fb_synth_model* model, int V, int dtype,
+                    int32_t* pred, void* logits, void* stream) {
+    int rc = check_logit_args(st, tokens, T_max, pack, model, V, dtype, pred, logits);
+    if (rc) return rc;
+    hipError_t e = fb::launch_synth_logits(st, tokens, T_max, pack, model, V, dtype, pred,
+                                           logits, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "synthetic logits launch");
+    return ok();
+}
+
+int fb_decode_loop(const fb_loop_args* a, int max_steps, int check_every, int use_graph,
+                   int* steps_out, int* done_out, void* stream) {
+    if (!a) return fail(FB_E_INVAL, "args is NULL");
+    if (max_steps < 0 || check_every < 1)
+        return fail(FB_E_INVAL, "need max_steps >= 0 and check_every >= 1");
+    hipStream_t s = (hipStream_t)stream;
+    if (use_graph && !s) return fail(FB_E_INVAL, "graph capture needs a non-null stream");
+    int rc = check_logit_args(a->st, a->tokens, a->T_max, a->pack, a->model, a->V,
+                              a->logit_dtype, a->pred, a->logits);
+    if (rc) return rc;
+    rc = check_update_args(a->pack, a->V, a->tokens, a->conf, a->argmax, a->st, a->pe, a->fin,
+                           a->prm, a->T_max, a->n_max);
+    if (rc) return rc;
+    if (a->prm->mask_id != a->V - 1)
+        return fail(FB_E_INVAL, "the synthetic model needs mask_id == V - 1");
+    if (!a->counters || !a->forwards) return fail(FB_E_INVAL, "counters or forwards is NULL");
+    const fb::UpdateSizes uz = fb::update_sizes(a->pack, a->V, cu_count());
+    rc = check_ws(a->upd_ws, a->upd_ws_bytes, uz.total);
+    if (rc) return rc;
+    fb::AttnPlanSizes az{};
+    if (a->shape) {
+        rc = check_embed_args(a->pack, a->shape, a->q, a->k_new, a->v_new);
+        if (rc) return rc;
+        if (!a->k_cache || !a->v_cache || !a->page_table || !a->attn_out)
+            return fail(FB_E_INVAL, "an attention pointer is NULL");
+        if (!aligned16(a->q) || !aligned16(a->k_new) || !aligned16(a->v_new) ||
+            !aligned16(a->k_cache) || !aligned16(a->v_cache) || !aligned16(a->attn_out))
+            return fail(FB_E_INVAL, "attention tensors must be 16-byte aligned");
+        az = fb::attention_sizes(a->pack, a->shape, cu_count());
+        if (a->attn_ws_bytes < az.total || (az.total > 0 && !a->attn_ws))
+            return fail(FB_E_WORKSPACE, "attention workspace has %zu bytes, needs %zu",
+                        a->attn_ws_bytes, az.total);
+        if (a->attn_ws && !aligned16(a->attn_ws))
+            return fail(FB_E_INVAL, "attention workspace must be 16-byte aligned");
+    }
+
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    auto cleanup = [&]() {
+        if (exec) (void)hipGraphExecDestroy(exec);
+        if (graph) (void)hipGraphDestroy(graph);
+    };
+    int enq = 0, done = 0;
+    hipError_t e = hipSuccess;
+    for (;;) {
+        if (enq >= max_steps) break;
+        const int k = check_every < max_steps - enq ? check_every : max_steps - enq;
+        if (use_graph && k == check_every) {
+            if (!exec) {
+                e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+                if (e != hipSuccess) return hip_fail(e, "begin capture");
+                hipError_t ee = hipSuccess;
+                for (int i = 0; i < k && ee == hipSuccess; ++i) ee = enqueue_step(a, &az, uz, s);
+                e = hipStreamEndCapture(s, &graph);
+                if (ee != hipSuccess) {
+                    cleanup();
+                    return hip_fail(ee, "step launch during capture");
+                }
+                if (e != hipSuccess) {
+                    cleanup();
+                    return hip_fail(e, "end capture");
+                }
+                e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+                if (e != hipSuccess) {
+                    exec = nullptr;
+                    cleanup();
+                    return hip_fail(e, "graph instantiate");
+                }
+            }
+            e = hipGraphLaunch(exec, s);
+            if (e != hipSuccess) {
+                cleanup();
+                return hip_fail(e, "graph launch");
+            }
+        } else {
+            for (int i = 0; i < k; ++i) {
+                e = enqueue_step(a, &az, uz, s);
+                if (e != hipSuccess) {
+                    cleanup();
+                    return hip_fail(e, "step launch");
+                }
+            }
+        }
+        enq += k;
+        e = fb::launch_loop_count(a->st, a->pack->B, a->counters, a->forwards, 0, s);
+        int32_t flag = 1;
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&flag, &a->counters->any_active, sizeof flag,
+                               hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) {
+            cleanup();
+            return hip_fail(e, "reading the loop flag");
+        }
+        if (!flag) {
+            done = 1;
+            break;
+        }
+    }
+    if (!done && enq == 0) {
+        // no step asked for: report the current state
+        int32_t flag = 1;
+        e = fb::launch_loop_count(a->st, a->pack->B, a->counters, a->forwards, 0, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&flag, &a->counters->any_active, sizeof flag,
+                               hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) {
+            cleanup();
+            return hip_fail(e, "reading the loop flag");
+        }
+        done = !flag;
+    }
+    cleanup();
+    if (steps_out) *steps_out = enq;
+    if (done_out) *done_out = done;
     return ok();
 }
 

@@ -208,7 +208,8 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
                int32_t* __restrict__ tokens, int T_max, float* __restrict__ conf_out,
                int32_t* __restrict__ argmax_out, fb_req_state* __restrict__ st,
                uint8_t* __restrict__ pe, uint8_t* __restrict__ fin, int n_max, int bl,
-               int W_max, UpdParams prm, fb_req_stats* __restrict__ stats) {
+               int W_max, UpdParams prm, fb_req_stats* __restrict__ stats,
+               double* __restrict__ rho_last) {
     extern __shared__ unsigned char upd_smem[];
     const int rows_cap = W_max * bl;
     float* s_conf = reinterpret_cast<float*>(upd_smem);
@@ -341,6 +342,13 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         rs.m2t += s_m2t[sl];
         rs.t2t += s_t2t[sl];
     }
+    if (prm.flags & FB_SYNC_WINDOW) {
+        // the shared window moves in sync_window_kernel, after every request
+        // has finished its blocks' bookkeeping
+        rho_last[b] = w > 0 ? s_rho[w - 1] : 0.0;
+        if (stats) stats[b] = rs;
+        return;
+    }
     fb_req_state ns = s;
     if (ns.active) {
         const uint8_t* fin_b = fin + (size_t)b * n_max;
@@ -389,6 +397,128 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
     if (stats) stats[b] = rs;
 }
 
+// Batch-synchronous retire and admit (FB_SYNC_WINDOW; the synchronous
+// wavefront of the Sec. 5 ablation): one workgroup over all requests.  The
+// requests taking part are the active, well-formed ones; they must share
+// (L, R, n).  Thread i owns requests i, i + blockDim.x, ... and is the only
+// writer of their state and statistics.
+constexpr int kSyncThreads = 1024;
+
+__global__ void __launch_bounds__(kSyncThreads)
+sync_window_kernel(PackView pv, int B, fb_req_state* __restrict__ st,
+                   const int32_t* __restrict__ tokens, int T_max,
+                   uint8_t* __restrict__ pe, uint8_t* __restrict__ fin, int n_max, int bl,
+                   UpdParams prm, fb_req_stats* __restrict__ stats,
+                   const double* __restrict__ rho_last) {
+    __shared__ int s_cnt, s_lo[3], s_hi[3], s_all;
+    __shared__ double s_min[kSyncThreads / 64];
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        s_cnt = 0;
+        for (int k = 0; k < 3; ++k) {
+            s_lo[k] = 0x7fffffff;
+            s_hi[k] = -0x7fffffff;
+        }
+    }
+    __syncthreads();
+    auto part = [&](int b) { return st[b].active != 0 && pv.req_w[b] >= 0; };
+    for (int b = tid; b < B; b += kSyncThreads) {
+        if (!part(b)) continue;
+        const fb_req_state s = st[b];
+        const int v[3] = {s.L, s.R, s.n_blocks};
+        atomicAdd(&s_cnt, 1);
+        for (int k = 0; k < 3; ++k) {
+            atomicMin(&s_lo[k], v[k]);
+            atomicMax(&s_hi[k], v[k]);
+        }
+    }
+    __syncthreads();
+    if (s_cnt == 0) return;
+    if (s_lo[0] != s_hi[0] || s_lo[1] != s_hi[1] || s_lo[2] != s_hi[2]) {
+        for (int b = tid; b < B; b += kSyncThreads)
+            if (part(b)) record_error(pv.hdr, b, FB_DERR_STATE);
+        return;
+    }
+    const int L0 = s_lo[0], R0 = s_lo[1], n = s_lo[2];
+
+    // ---- retire: block L goes when every taking-part request finished it --
+    int L = L0;
+    while (L < R0) {
+        if (tid == 0) s_all = 1;
+        __syncthreads();
+        for (int b = tid; b < B; b += kSyncThreads)
+            if (part(b) && !fin[(size_t)b * n_max + L]) s_all = 0;
+        __syncthreads();
+        const int all = s_all;
+        __syncthreads();
+        if (!all) break;
+        for (int b = tid; b < B; b += kSyncThreads) {
+            if (!part(b)) continue;
+            fb_req_state s = st[b];
+            s.L = L + 1;
+            int eos = 0;
+            if (prm.eos_id >= 0) {
+                const int32_t* blk = tokens + (size_t)b * T_max + s.gen_start + L * bl;
+                for (int i = 0; i < bl; ++i) eos |= blk[i] == prm.eos_id;
+            }
+            if (eos) {
+                s.active = 0;
+                s.eos_hit = 1;
+            }
+            st[b] = s;
+            if (stats) {
+                stats[b].committed += 1;
+                if (eos) {
+                    stats[b].eos = 1;
+                    stats[b].done = 1;
+                }
+            }
+        }
+        L += 1;
+        __syncthreads();
+    }
+    if (L >= n) {
+        for (int b = tid; b < B; b += kSyncThreads) {
+            if (!part(b)) continue;
+            st[b].active = 0;
+            if (stats) stats[b].done = 1;
+        }
+        return;
+    }
+
+    // ---- admit, gated by the smallest readiness of B_{R-1} ------------------
+    int R = R0;
+    auto admit = [&]() {
+        for (int b = tid; b < B; b += kSyncThreads) {
+            if (!part(b)) continue;
+            pe[(size_t)b * n_max + R] = 0;
+            fin[(size_t)b * n_max + R] = 0;
+            if (stats) stats[b].spawned += 1;
+        }
+        R += 1;
+    };
+    if (L == R && R < n) admit();
+    while (R - L < prm.W && R < n) {
+        const int g = R - 1;
+        double m = 2.0;    // above any readiness
+        for (int b = tid; b < B; b += kSyncThreads) {
+            if (!part(b)) continue;
+            const double rho = g < L ? 1.0 : (g < R0 ? rho_last[b] : 0.0);
+            m = fmin(m, rho);
+        }
+        for (int off = 32; off > 0; off >>= 1) m = fmin(m, __shfl_xor(m, off, 64));
+        if ((tid & 63) == 0) s_min[tid >> 6] = m;
+        __syncthreads();
+        double mm = s_min[0];
+        for (int k = 1; k < kSyncThreads / 64; ++k) mm = fmin(mm, s_min[k]);
+        __syncthreads();
+        if (!(mm >= prm.theta)) break;
+        admit();
+    }
+    for (int b = tid; b < B; b += kSyncThreads)
+        if (part(b)) st[b].R = R;
+}
+
 }  // namespace
 
 UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count) {
@@ -404,7 +534,8 @@ UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count) {
     chunk = (chunk + 7) / 8 * 8;
     z.nsplit = (V + chunk - 1) / chunk;
     z.chunk = chunk;
-    z.total = (size_t)pack->row_cap * z.nsplit * sizeof(float4);
+    z.off_rho = (size_t)pack->row_cap * z.nsplit * sizeof(float4);
+    z.total = z.off_rho + ((size_t)pack->B * sizeof(double) + 15) / 16 * 16;
     return z;
 }
 
@@ -436,10 +567,19 @@ hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax
                   p->eos_id,   p->S_pe,     p->W,           p->flags};
     const size_t rows_cap = (size_t)pack->W_max * pack->bl;
     const size_t smem = rows_cap * (sizeof(float) + sizeof(int) + 1);
+    double* rho_last = reinterpret_cast<double*>(static_cast<char*>(const_cast<void*>(ws)) +
+                                                 z.off_rho);
     hipLaunchKernelGGL(request_kernel, dim3(pack->B), dim3(kUpdThreads), smem, stream,
                        static_cast<const float4*>(ws), z.nsplit, pv, tokens, T_max,
                        conf, argmax, st, pe, fin, n_max, pack->bl, pack->W_max, prm,
-                       stats);
+                       stats, rho_last);
+    if (p->flags & FB_SYNC_WINDOW) {
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(sync_window_kernel, dim3(1), dim3(kSyncThreads), 0, stream, pv,
+                           pack->B, st, tokens, T_max, pe, fin, n_max, pack->bl, prm,
+                           stats, rho_last);
+    }
     return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "flowblock.h"
+#include "flowblock_loop.h"
 
 namespace fb {
 
@@ -79,6 +80,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
 struct UpdateSizes {
     int nsplit;      // vocabulary partitions per row in the first pass
     int chunk;       // elements per partition (multiple of 8)
+    size_t off_rho;  // per-request readiness of the window's last block
     size_t total;    // workspace bytes
 };
 UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count);
@@ -90,5 +92,18 @@ hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax
                         const fb_pack* pack, const fb_update_params* prm,
                         fb_req_stats* stats, const void* ws, const UpdateSizes& sz,
                         hipStream_t stream);
+
+struct SynthSizes {
+    int nsplit;      // vocabulary partitions per row of the logits fill
+    int chunk;       // elements per partition (multiple of 8)
+};
+SynthSizes synth_sizes(const fb_pack* pack, int V);
+hipError_t launch_synth_logits(const fb_req_state* st, const int32_t* tokens, int T_max,
+                               const fb_pack* pack, const fb_synth_model* m, int V,
+                               int dtype, int32_t* pred, void* logits, hipStream_t stream);
+hipError_t launch_synth_embed(const fb_pack* pack, const fb_attn_shape* sh, uint64_t seed,
+                              void* q, void* k_new, void* v_new, hipStream_t stream);
+hipError_t launch_loop_count(const fb_req_state* st, int B, fb_loop_counters* counters,
+                             int32_t* forwards, int count, hipStream_t stream);
 
 }  // namespace fb

@@ -309,3 +309,51 @@ def state_from_records(rec):
                 L=rec[:, 3].astype(np.int64), R=rec[:, 4].astype(np.int64),
                 active=rec[:, 5].astype(np.int64),
                 eos_hit=rec[:, 6].astype(np.int64))
+
+
+# ------------------------------------------------------- multi-step loop ----
+def loop_levels(V, targets=(0.3, 0.85, 0.955, 0.99)):
+    """Peak heights of the synthetic model for vocabulary V: the logit a whose
+    two-level confidence e^a / (e^a + V - 1) is near each target, rounded to a
+    multiple of 1/8 (exact in bf16 below 32).  The default targets sit far from
+    the thresholds 0.9 / 0.8 the workloads use."""
+    out = []
+    for p in targets:
+        a = np.log(p / (1.0 - p) * (V - 1))
+        out.append(float(np.round(a * 8.0) / 8.0))
+    return tuple(out)
+
+
+def make_loop_host_state(B, prompts, n_blocks, bl, V, page_size, seed=0):
+    """Fresh requests for a whole decode: request b has a random prompt of
+    prompts[b] tokens (never the mask id V - 1), then n_blocks masked blocks
+    starting at gen_start = prompt length; L = 0, R = 1 (B_0 admitted), pe =
+    fin = 0.  Pages cover each request's full length, ids a seeded
+    permutation.  Same dict layout as ``make_host_state``."""
+    rng = _rng(seed, 11)
+    M = V - 1
+    prompts = np.asarray(prompts, dtype=np.int64)
+    assert len(prompts) == B
+    T_need = prompts + n_blocks * bl
+    T_max = int(-(-T_need.max() // page_size) * page_size)
+    tokens = np.full((B, T_max), M, dtype=np.int64)
+    for b in range(B):
+        tokens[b, :prompts[b]] = rng.integers(0, M, size=prompts[b])
+    pages_per_req = -(-T_need // page_size)
+    num_pages = int(pages_per_req.sum())
+    max_pages = int(pages_per_req.max())
+    perm = rng.permutation(num_pages)
+    page_table = np.full((B, max_pages), -1, dtype=np.int64)
+    k = 0
+    for b in range(B):
+        page_table[b, :pages_per_req[b]] = perm[k:k + pages_per_req[b]]
+        k += pages_per_req[b]
+    state = dict(gen_start=prompts.copy(), prompt_len=prompts.copy(),
+                 n_blocks=np.full(B, n_blocks, dtype=np.int64),
+                 L=np.zeros(B, dtype=np.int64), R=np.ones(B, dtype=np.int64),
+                 active=np.ones(B, dtype=np.int64), eos_hit=np.zeros(B, dtype=np.int64))
+    return dict(state=state, tokens=tokens,
+                pe=np.zeros((B, n_blocks), dtype=np.int64),
+                fin=np.zeros((B, n_blocks), dtype=np.int64),
+                page_table=page_table, num_pages=num_pages, T_max=T_max,
+                n_max=n_blocks, max_pages=max_pages)

@@ -1,7 +1,7 @@
-"""The C ABI library loads, exports every function include/flowblock.h
-declares, and rejects bad host-visible arguments before touching a GPU.
+"""The C ABI library loads, exports every function include/*.h declares, and rejects bad host-visible arguments before touching a GPU.
 CPU only: nothing here launches a kernel."""
 import ctypes
+import glob
 import os
 import re
 import subprocess
@@ -11,13 +11,15 @@ import pytest
 from paper_2607_17652_amd import binding as fb
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "flowblock.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(fb_\w+)\s*\(", src, re.M)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(fb_\w+)\s*\(", src, re.M))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -56,6 +58,35 @@ def test_struct_sizes_match_header():
     assert ctypes.sizeof(fb.fb_update_params) == 56
     assert fb.REQ_STATE_DTYPE.itemsize == 32
     assert fb.REQ_STATS_DTYPE.itemsize == 40
+    assert ctypes.sizeof(fb.fb_synth_model) == 24
+
+
+def test_ctypes_layouts_match_the_c_compiler(tmp_path):
+    """Every struct the binding mirrors has the size and field offsets the C
+    compiler gives the header's declaration."""
+    structs = [fb.fb_pack, fb.fb_pack_offsets, fb.fb_attn_shape,
+               fb.fb_update_params, fb.fb_synth_model, fb.fb_loop_args]
+    lines = ["#include <stdio.h>", "#include <stddef.h>",
+             '#include "flowblock_loop.h"', "int main(void) {"]
+    for S in structs:
+        n = S.__name__
+        lines.append(f'printf("{n} %zu\\n", sizeof({n}));')
+        for f, _ in S._fields_:
+            lines.append(f'printf("{n}.{f} %zu\\n", offsetof({n}, {f}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src),
+                    "-o", str(exe)], check=True)
+    got = dict(l.rsplit(" ", 1) for l in
+               subprocess.run([str(exe)], capture_output=True, text=True,
+                              check=True).stdout.split("\n") if l)
+    for S in structs:
+        n = S.__name__
+        assert int(got[n]) == ctypes.sizeof(S), n
+        for f, _ in S._fields_:
+            assert int(got[f"{n}.{f}"]) == getattr(S, f).offset, (n, f)
 
 
 def _init(lib, buf, nbytes, B, W, bl, layout):
