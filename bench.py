@@ -10,7 +10,9 @@ same request state, so all K steps do identical work.
 Prints ONE JSON line: active tokens/s (live window tokens, never padding),
 attention % of dense bf16 MFMA peak, update HBM GB/s, per-phase times from
 HIP events recorded on the launch stream, a roofline entry for the dominant
-kernel and the fp64 oracle timed on a bounded sample on the host cores.
+kernel, the fp64 oracle timed on a bounded sample on the host cores, and
+whole decodes on the synthetic model (serial, HWP and the batch-synchronous
+window) under "loop".
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload serve256]
 """
@@ -42,6 +44,8 @@ def parse_args():
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay of the K steps")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--no-loop", action="store_true",
+                    help="skip the whole-decode loop runs on the synthetic model")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -226,6 +230,64 @@ def graph_replay(torch, fb, step, one_step, copies, K, W):
             "steps_per_replay": K}
 
 
+LOOP_WORKLOAD = dict(name="loop64", B=64, prompt=(256, 1024), n_blocks=16, bl=32,
+                     W_max=4, V=157184, Hq=32, Hkv=8, d=128, seed=0)
+
+
+def loop_bench(torch, fb, synth, DecodeLoop):
+    """Whole decodes (Alg. 1's outer loop on the device) of 64 requests on the
+    synthetic model: serial (W = 1), HWP (W = 4) and the batch-synchronous
+    window (W = 4), each timed around one fb_decode_loop call (steps replayed
+    as a HIP graph, one flag read per 16 steps).  Every step runs the full
+    path: pack, synthetic embeddings, window KV write, attention, synthetic
+    logits over the whole vocabulary, vocab reduction and update."""
+    import numpy as np
+    c = LOOP_WORKLOAD
+    rng = np.random.default_rng(c["seed"])
+    prompts = rng.integers(c["prompt"][0], c["prompt"][1] + 1, size=c["B"])
+    host0 = synth.make_loop_host_state(c["B"], prompts, c["n_blocks"], c["bl"], c["V"],
+                                       page_size=c["bl"], seed=c["seed"])
+    P = host0["num_pages"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(c["seed"] + 17)
+    k_cache = (torch.randn((P, c["Hkv"], c["bl"], c["d"]), generator=gen, device="cuda")
+               * 0.1).to(torch.bfloat16)
+    v_cache = (torch.randn((P, c["Hkv"], c["d"], c["bl"]), generator=gen, device="cuda")
+               * 0.1).to(torch.bfloat16)
+    levels = synth.loop_levels(c["V"])
+    gen_tokens = c["B"] * c["n_blocks"] * c["bl"]
+    runs = {}
+    for name, W, sync in (("serial", 1, False), ("hwp", 4, False), ("sync", 4, True)):
+        prm = dict(tau_mask=0.9, tau_edit=0.8, theta=0.5, mask_id=c["V"] - 1, eos_id=-1,
+                   S_pe=2, W=W, edit_masked=False, force_progress=False, sync_window=sync)
+        attn = dict(Hq=c["Hq"], Hkv=c["Hkv"], d=c["d"], dtype="bf16", page_size=c["bl"],
+                    k_cache=k_cache, v_cache=v_cache, embed_seed=c["seed"] + 5)
+        loop = DecodeLoop(host0, c["bl"], c["W_max"], c["V"], prm, c["seed"] + 99, levels,
+                          attn=attn)
+        stream = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        enq, done = loop.run(max_steps=4096, check_every=16, use_graph=True, stream=stream)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        if not done:
+            raise RuntimeError(f"loop {name} did not finish in 4096 steps")
+        r = loop.results()
+        fw = r["forwards"].astype(np.float64)
+        runs[name] = {"W": W, "sync_window": sync, "steps": r["steps"],
+                      "steps_enqueued": enq, "ms": dt * 1e3,
+                      "ms_per_step": dt * 1e3 / max(enq, 1),
+                      "tokens_per_s": gen_tokens / dt,
+                      "tpf_mean": float(np.mean(c["n_blocks"] * c["bl"] / fw))}
+        print(f"[bench] loop {name}: {r['steps']} steps, {dt * 1e3:.1f} ms",
+              file=sys.stderr, flush=True)
+        del loop
+    return {"workload": {k: v for k, v in c.items()}, "generated_tokens": gen_tokens,
+            "runs": runs,
+            "hwp_over_serial": runs["hwp"]["tokens_per_s"] / runs["serial"]["tokens_per_s"],
+            "hwp_over_sync": runs["hwp"]["tokens_per_s"] / runs["sync"]["tokens_per_s"]}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -240,7 +302,7 @@ def main():
     import torch
     from paper_2607_17652_amd import binding as fb
     from paper_2607_17652_amd import synth
-    from paper_2607_17652_amd.runner import WavefrontStep
+    from paper_2607_17652_amd.runner import DecodeLoop, WavefrontStep
 
     torch.cuda.set_device(0)
     wl = synth.workload(args.workload)
@@ -340,6 +402,9 @@ def main():
     }
     if graph is not None:
         out["graph"] = graph
+    if not args.no_loop:
+        del copies
+        out["loop"] = loop_bench(torch, fb, synth, DecodeLoop)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
