@@ -310,6 +310,28 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens,
 int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack,
                     void* ws, size_t ws_bytes, void* stream);
 
+/* Workspace bytes of fb_lmhead_reduce (its own partials) for this pack,
+ * vocabulary and hidden size; 0 if the arguments are invalid. */
+size_t fb_lmhead_workspace_bytes(const fb_pack* pack, int V, int D);
+
+/* The model's last layer and step 1's reduction in one pass: the logits of
+ * the forward in Alg. 1, Z = hidden . weight^T, are reduced per live row to
+ * x_hat and the partials of p exactly as fb_vocab_reduce would reduce them,
+ * without Z ever being written to memory.  The result goes to the update
+ * workspace `upd_ws` in the form fb_denoise_apply reads, so
+ * fb_lmhead_reduce + fb_denoise_apply is fb_denoise_update on logits that
+ * never exist.  The logits are accumulated in float32 (MFMA bf16 products),
+ * so they may differ from an exact product by the accumulation error.
+ *   hidden  bf16 [row_cap][D] (the packed rows' final hidden states)
+ *   weight  bf16 [V][D] (one row per vocabulary id)
+ *   D       a multiple of 64; V * D and row_cap * D below 2^30
+ *   lm_ws   device workspace of fb_lmhead_workspace_bytes bytes
+ *   upd_ws  the update workspace of fb_update_workspace_bytes(pack, V) bytes
+ * Rows that are not live are not reduced. */
+int fb_lmhead_reduce(const void* hidden, const void* weight, int D, int V,
+                     const fb_pack* pack, void* lm_ws, size_t lm_ws_bytes, void* upd_ws,
+                     size_t upd_ws_bytes, void* stream);
+
 /* fb_denoise_apply: steps 1 (merge of the partials: x_hat, p) through 5 of
  * fb_denoise_update, from the workspace fb_vocab_reduce filled for the same
  * pack and V. */

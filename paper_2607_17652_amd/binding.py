@@ -42,6 +42,7 @@ EXPORTS = [
     "fb_wavefront_attention", "fb_update_workspace_bytes", "fb_denoise_update",
     "fb_vocab_reduce", "fb_denoise_apply",
     "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
+    "fb_lmhead_workspace_bytes", "fb_lmhead_reduce",
 ]
 
 
@@ -144,6 +145,8 @@ def lib():
             "fb_denoise_apply": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, i32,
                                        P(fb_pack), P(fb_update_params), vp, vp, sz,
                                        vp]),
+            "fb_lmhead_workspace_bytes": (sz, [P(fb_pack), i32, i32]),
+            "fb_lmhead_reduce": (i32, [vp, vp, i32, i32, P(fb_pack), vp, sz, vp, sz, vp]),
             "fb_synth_embed": (i32, [P(fb_pack), P(fb_attn_shape), ctypes.c_uint64,
                                      vp, vp, vp, vp]),
             "fb_synth_logits": (i32, [vp, vp, i32, P(fb_pack), P(fb_synth_model),
@@ -337,6 +340,20 @@ def fb_denoise_apply(V, tokens, conf, argmax, st, pe, fin, pack, params, stats, 
                                   _ptr(argmax), _ptr(st), _ptr(pe), _ptr(fin),
                                   pe.shape[-1], pack.ref(), ctypes.byref(params),
                                   _ptr(stats), _ptr(ws), nbytes, _stream(stream)))
+
+
+def fb_lmhead_workspace_bytes(pack, V, D):
+    return int(lib().fb_lmhead_workspace_bytes(pack.ref(), V, D))
+
+
+def fb_lmhead_reduce(hidden, weight, pack, lm_ws, upd_ws, stream=None):
+    """hidden bf16 [row_cap, D]; weight bf16 [V, D]; the reduction lands in
+    upd_ws for fb_denoise_apply."""
+    D = hidden.shape[-1]
+    V = weight.shape[0]
+    _check(lib().fb_lmhead_reduce(_ptr(hidden), _ptr(weight), D, V, pack.ref(), _ptr(lm_ws),
+                                  lm_ws.numel() * lm_ws.element_size(), _ptr(upd_ws),
+                                  upd_ws.numel() * upd_ws.element_size(), _stream(stream)))
 
 
 def stats_to_numpy(stats_tensor, B):

@@ -277,6 +277,48 @@ int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack, v
     return ok();
 }
 
+namespace {
+
+int check_lmhead(const fb_pack* pack, int V, int D) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
+    if (D < 64 || D % 64)
+        return fail(FB_E_UNSUPPORTED, "hidden size %d must be a positive multiple of 64", D);
+    if ((long long)V * D >= (1LL << 30) || (long long)pack->row_cap * D >= (1LL << 30))
+        return fail(FB_E_UNSUPPORTED, "V*D and row_cap*D must be below 2^30");
+    return FB_OK;
+}
+
+}  // namespace
+
+size_t fb_lmhead_workspace_bytes(const fb_pack* pack, int V, int D) {
+    if (check_lmhead(pack, V, D)) return 0;
+    return fb::lm_sizes(pack, V, D, cu_count()).total;
+}
+
+int fb_lmhead_reduce(const void* hidden, const void* weight, int D, int V, const fb_pack* pack,
+                     void* lm_ws, size_t lm_ws_bytes, void* upd_ws, size_t upd_ws_bytes,
+                     void* stream) {
+    int rc = check_lmhead(pack, V, D);
+    if (rc) return rc;
+    if (!hidden || !weight) return fail(FB_E_INVAL, "hidden or weight is NULL");
+    if (!aligned16(hidden) || !aligned16(weight))
+        return fail(FB_E_INVAL, "hidden and weight must be 16-byte aligned");
+    const fb::LmSizes z = fb::lm_sizes(pack, V, D, cu_count());
+    if (lm_ws_bytes < z.total || !lm_ws)
+        return fail(FB_E_WORKSPACE, "LM-head workspace has %zu bytes, needs %zu", lm_ws_bytes,
+                    z.total);
+    if (!aligned16(lm_ws)) return fail(FB_E_INVAL, "LM-head workspace must be 16-byte aligned");
+    const fb::UpdateSizes uz = fb::update_sizes(pack, V, cu_count());
+    rc = check_ws(upd_ws, upd_ws_bytes, uz.total);
+    if (rc) return rc;
+    hipError_t e = fb::launch_lmhead(hidden, weight, D, V, pack, lm_ws, z, upd_ws, uz,
+                                     (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "LM-head launch");
+    return ok();
+}
+
 int fb_denoise_apply(int V, int32_t* tokens, int T_max, float* conf, int32_t* argmax,
                      fb_req_state* st, uint8_t* pe, uint8_t* fin, int n_max,
                      const fb_pack* pack, const fb_update_params* prm,

@@ -12,44 +12,13 @@
 //                     then retires and admits on one thread.
 // Every reduction has a fixed order, so results are bit-reproducible.
 #include "internal.h"
+#include "top.h"
 
 namespace fb {
 namespace {
 
 constexpr int kVocabThreads = 256;
 constexpr int kUpdThreads = 256;
-constexpr float kLog2e = 1.4426950408889634f;
-
-// Running (max, index, scaled sum).  `s` is relative to mL = round(m*log2e).
-struct Top {
-    float m;
-    float mL;
-    float s;
-    int idx;
-};
-
-__device__ inline Top top_empty() { return Top{-INFINITY, -INFINITY, 0.f, 0x7fffffff}; }
-
-// The reference mL must be the rounded product everywhere it is used: with
-// contraction, `x - m*log2e` would become an fma on the exact product and
-// every merge would scale the sum by the product's rounding error.
-__device__ inline float scaled_ref(float m) {
-#pragma clang fp contract(off)
-    return m * kLog2e;
-}
-
-// Order-independent merge of two partial results (commutative bit for bit).
-__device__ inline Top top_merge(const Top& a, const Top& b) {
-#pragma clang fp contract(off)
-    if (a.m == -INFINITY) return b;
-    if (b.m == -INFINITY) return a;
-    Top r;
-    r.m = fmaxf(a.m, b.m);
-    r.mL = scaled_ref(r.m);
-    r.s = a.s * __builtin_amdgcn_exp2f(a.mL - r.mL) + b.s * __builtin_amdgcn_exp2f(b.mL - r.mL);
-    r.idx = a.m > b.m ? a.idx : (b.m > a.m ? b.idx : min(a.idx, b.idx));
-    return r;
-}
 
 // Fold n consecutive values starting at index v into t (values in index order).
 template <int N>

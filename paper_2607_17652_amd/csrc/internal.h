@@ -93,6 +93,18 @@ hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax
                         fb_req_stats* stats, const void* ws, const UpdateSizes& sz,
                         hipStream_t stream);
 
+struct LmSizes {
+    int n_rtiles;        // 256-token tiles over row_cap
+    int n_vtiles;        // 256-id vocabulary tiles
+    int tiles_per_part;  // vocabulary tiles per partition
+    int P;               // partitions (partials per row)
+    size_t total;        // workspace bytes (row_cap * P partials)
+};
+LmSizes lm_sizes(const fb_pack* pack, int V, int D, int cu_count);
+hipError_t launch_lmhead(const void* hidden, const void* weight, int D, int V,
+                         const fb_pack* pack, void* lm_ws, const LmSizes& z, void* upd_ws,
+                         const UpdateSizes& uz, hipStream_t stream);
+
 struct SynthSizes {
     int nsplit;      // vocabulary partitions per row of the logits fill
     int chunk;       // elements per partition (multiple of 8)

@@ -1,0 +1,303 @@
+// LM head with the vocabulary reduction as its epilogue: the last layer of
+// the forward f_theta of Alg. 1, Z = H W^T, reduced per row to the symbols of
+// Eq. 1 (max, lowest index of the max, sum of exponentials) without the
+// logits ever reaching memory.
+//
+// lmhead_kernel   one workgroup of 8 waves per (256-row token tile, vocabulary
+//                 partition).  It walks the partition's 256-id vocabulary
+//                 tiles; for each, Z^T tile = W_tile . H_tile^T on
+//                 v_mfma_f32_32x32x16_bf16 over K = D in 64-wide stages
+//                 (double-buffered LDS, filled by direct global->LDS loads
+//                 with a scalar base and a per-lane offset fixed for the
+//                 whole kernel), then folds the tile into a running
+//                 (max, index, scaled sum) per token.  Wave (wv, wt) owns
+//                 vocabulary rows wv*128.. and tokens wt*64.. of the tile.
+//                 With Z^T in the accumulators each lane holds one token and
+//                 16 vocabulary ids per MFMA tile, so the per-token reduction
+//                 is mostly in-lane.
+// lm_merge_kernel one wave per row: merges the row's partition partials in a
+//                 fixed order into the first partial of the update workspace
+//                 (the rest are set empty), the input of the update kernel.
+#include "internal.h"
+#include "top.h"
+
+namespace fb {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kLmThreads = 512;                   // 8 waves
+constexpr int kTileV = 256;                       // vocabulary ids per tile
+constexpr int kTileT = 256;                       // tokens per tile
+constexpr int kBK = 64;                           // K per stage
+constexpr int kRowBytes = kBK * 2;                // 128 B: one row of a stage
+constexpr int kHalfBytes = kTileV * kRowBytes;    // 32 KB: W part of a stage
+constexpr int kStageBytes = 2 * kHalfBytes;       // W part, then H part
+constexpr int kStages = 2;
+constexpr int kMergeThreads = 256;
+
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ inline void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__global__ void __launch_bounds__(kLmThreads, 1)
+lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int D, int V,
+              int row_cap, int n_rtiles, int n_vtiles, int tiles_per_part, int P,
+              PackView pv, float4* __restrict__ part) {
+    __shared__ __attribute__((aligned(16))) unsigned char lds[kStages * kStageBytes];
+    __shared__ Top s_top[kTileT];
+    __shared__ int s_live;
+
+    const int tid = threadIdx.x;
+    const int rt = blockIdx.x % n_rtiles;
+    const int pidx = blockIdx.x / n_rtiles;
+    const int row0 = rt * kTileT;
+    const int vt0 = pidx * tiles_per_part;
+    const int vt1 = min(n_vtiles, vt0 + tiles_per_part);
+    if (vt0 >= vt1) return;
+    // skip token tiles without a live row
+    if (tid == 0) s_live = 0;
+    __syncthreads();
+    if (tid < kTileT && row0 + tid < row_cap && pv.row_req[row0 + tid] >= 0) s_live = 1;
+    __syncthreads();
+    if (!s_live) return;
+
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int n = lane & 31;
+    const int h = lane >> 5;
+    const int wv = wave & 1;          // vocabulary half of the tile
+    const int wt = wave >> 1;         // token quarter of the tile
+
+    // ---- DMA assignment: wave w fills W rows [32w, 32w+32) and H rows
+    // [32w, 32w+32) of each stage, 8 rows (1 KB) per instruction; lane L
+    // writes LDS chunk L%8 of row L/8, which holds logical K chunk
+    // (L%8) ^ (row%8) -- the swizzle that makes the operand reads
+    // conflict-free.
+    const int lrow = lane >> 3;
+    const int lchunk = (lane & 7) ^ lrow;            // row % 8 == lrow
+    uint32_t h_off[4];
+    int w_row[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = wave * 32 + j * 8 + lrow;
+        const int tr = min(row0 + r, row_cap - 1);
+        h_off[j] = (uint32_t)(((size_t)tr * D + lchunk * 8) * 2);
+        w_row[j] = r;
+    }
+    uint32_t m0_w[4], m0_h[4];
+    const uint32_t lds_base = (uint32_t)(uintptr_t)&lds[0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        m0_w[j] = __builtin_amdgcn_readfirstlane(lds_base + (wave * 4 + j) * 1024);
+        m0_h[j] = __builtin_amdgcn_readfirstlane(lds_base + kHalfBytes + (wave * 4 + j) * 1024);
+    }
+    uint32_t w_off[4];
+    auto set_vtile = [&](int vt) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int vr = min(vt * kTileV + w_row[j], V - 1);
+            w_off[j] = (uint32_t)(((size_t)vr * D + lchunk * 8) * 2);
+        }
+    };
+    const int KS = D / kBK;
+    const int n_it = (vt1 - vt0) * KS;
+    // issue iteration `it` (vocabulary tile vt0 + it/KS, K step it%KS) into `stage`
+    auto issue = [&](int it, int stage) {
+        const int k0 = (it % KS) * kBK;
+        const uint16_t* wb = W + k0;
+        const uint16_t* hb = H + k0;
+        const uint32_t so = stage * kStageBytes;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(m0_w[j] + so), "v"(w_off[j]), "s"(wb) : "memory");
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(m0_h[j] + so), "v"(h_off[j]), "s"(hb) : "memory");
+    };
+
+    // operand reads: row r of a stage part, logical chunk 2kk + h
+    const uint32_t swz = (uint32_t)((h ^ (n & 7)) * 16);
+    const uint32_t a_row = (uint32_t)((wv * 128 + n) * kRowBytes);
+    const uint32_t b_row = (uint32_t)(kHalfBytes + (wt * 64 + n) * kRowBytes);
+
+    floatx16 acc[4][2];
+#pragma unroll
+    for (int vi = 0; vi < 4; ++vi)
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
+    Top top[2] = {top_empty(), top_empty()};
+
+    auto compute = [&](int stage) {
+        const unsigned char* st = lds + stage * kStageBytes;
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            const uint32_t ko = swz ^ (uint32_t)(kk << 5);
+            bf16x8 a[4], b[2];
+#pragma unroll
+            for (int vi = 0; vi < 4; ++vi)
+                a[vi] = *reinterpret_cast<const bf16x8*>(st + a_row + vi * 32 * kRowBytes + ko);
+#pragma unroll
+            for (int ti = 0; ti < 2; ++ti)
+                b[ti] = *reinterpret_cast<const bf16x8*>(st + b_row + ti * 32 * kRowBytes + ko);
+#pragma unroll
+            for (int vi = 0; vi < 4; ++vi)
+#pragma unroll
+                for (int ti = 0; ti < 2; ++ti)
+                    acc[vi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[vi], b[ti],
+                                                                          acc[vi][ti], 0, 0, 0);
+        }
+    };
+
+    // fold the finished tile vt into the running tops; lane value (vi, r)
+    // is vocabulary id vt*256 + wv*128 + vi*32 + (r/4)*8 + h*4 + r%4 --
+    // increasing in (vi, r), so the first maximum in that order is the
+    // lowest id.
+    auto fold = [&](int vt) {
+        const int vbase = vt * kTileV + wv * 128 + h * 4;
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) {
+            float f[64];
+#pragma unroll
+            for (int vi = 0; vi < 4; ++vi)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int v = vbase + vi * 32 + (r >> 2) * 8 + (r & 3);
+                    f[vi * 16 + r] = v < V ? acc[vi][ti][r] : -INFINITY;
+                }
+            float vmax = f[0];
+#pragma unroll
+            for (int j = 1; j < 64; ++j) vmax = fmaxf(vmax, f[j]);
+            Top& t = top[ti];
+            if (vmax > t.m) {
+#pragma clang fp contract(off)
+                int j0 = 63;
+#pragma unroll
+                for (int j = 63; j >= 0; --j)
+                    if (f[j] == vmax) j0 = j;
+                const float nmL = scaled_ref(vmax);
+                t.s *= __builtin_amdgcn_exp2f(t.mL - nmL);
+                t.m = vmax;
+                t.mL = nmL;
+                t.idx = vbase + (j0 >> 4) * 32 + ((j0 & 15) >> 2) * 8 + (j0 & 3);
+            }
+            if (t.m != -INFINITY) {
+                float e[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < 64; ++j)
+                    e[j & 3] += __builtin_amdgcn_exp2f(fmaf(f[j], kLog2e, -t.mL));
+                t.s += (e[0] + e[1]) + (e[2] + e[3]);
+            }
+        }
+#pragma unroll
+        for (int vi = 0; vi < 4; ++vi)
+#pragma unroll
+            for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
+    };
+
+    // ---- main loop: double-buffered stages over the flattened (tile, K step)
+    set_vtile(vt0);
+    issue(0, 0);
+    for (int it = 0; it < n_it; ++it) {
+        const int stage = it & 1;
+        wait_vm0();
+        lds_barrier();             // stage `it` landed; stage it-1 is free
+        if (it + 1 < n_it) {
+            if ((it + 1) % KS == 0) set_vtile(vt0 + (it + 1) / KS);
+            issue(it + 1, stage ^ 1);
+        }
+        compute(stage);
+        if (it % KS == KS - 1) fold(vt0 + it / KS);
+    }
+
+    // ---- merge: lane halves, then the two vocabulary halves of each token
+#pragma unroll
+    for (int ti = 0; ti < 2; ++ti) {
+        Top o;
+        o.m = __shfl_xor(top[ti].m, 32, 64);
+        o.mL = __shfl_xor(top[ti].mL, 32, 64);
+        o.s = __shfl_xor(top[ti].s, 32, 64);
+        o.idx = __shfl_xor(top[ti].idx, 32, 64);
+        top[ti] = top_merge(top[ti], o);
+    }
+    __syncthreads();
+    if (wv == 1 && h == 0) {
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) s_top[wt * 64 + ti * 32 + n] = top[ti];
+    }
+    __syncthreads();
+    if (wv == 0 && h == 0) {
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti) {
+            const int tok = wt * 64 + ti * 32 + n;
+            const int row = row0 + tok;
+            const Top t = top_merge(top[ti], s_top[tok]);
+            if (row < row_cap && pv.row_req[row] >= 0)
+                part[(size_t)row * P + pidx] = top_pack(t);
+        }
+    }
+}
+
+// One wave per row: partials k = lane, lane + 64, ... merged per lane in
+// increasing k, then across lanes by a fixed butterfly.
+__global__ void __launch_bounds__(kMergeThreads)
+lm_merge_kernel(const float4* __restrict__ lm_part, int P, PackView pv, int row_cap,
+                float4* __restrict__ upd_part, int nsplit) {
+    const int row = blockIdx.x * (kMergeThreads / 64) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= row_cap || pv.row_req[row] < 0) return;
+    Top t = top_empty();
+    for (int k = lane; k < P; k += 64) t = top_merge(t, top_unpack(lm_part[(size_t)row * P + k]));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        Top o;
+        o.m = __shfl_xor(t.m, off, 64);
+        o.mL = __shfl_xor(t.mL, off, 64);
+        o.s = __shfl_xor(t.s, off, 64);
+        o.idx = __shfl_xor(t.idx, off, 64);
+        t = top_merge(t, o);
+    }
+    for (int k = lane; k < nsplit; k += 64)
+        upd_part[(size_t)row * nsplit + k] = top_pack(k == 0 ? t : top_empty());
+}
+
+}  // namespace
+
+LmSizes lm_sizes(const fb_pack* pack, int V, int D, int cu_count) {
+    LmSizes z{};
+    z.n_rtiles = (pack->row_cap + kTileT - 1) / kTileT;
+    z.n_vtiles = (V + kTileV - 1) / kTileV;
+    // about 8 workgroups per compute unit over the token tiles' partitions
+    const int target = 8 * (cu_count > 0 ? cu_count : 256);
+    int P = (target + z.n_rtiles - 1) / z.n_rtiles;
+    if (P > z.n_vtiles) P = z.n_vtiles;
+    if (P < 1) P = 1;
+    z.tiles_per_part = (z.n_vtiles + P - 1) / P;
+    z.P = (z.n_vtiles + z.tiles_per_part - 1) / z.tiles_per_part;
+    z.total = (size_t)pack->row_cap * z.P * sizeof(float4);
+    (void)D;
+    return z;
+}
+
+hipError_t launch_lmhead(const void* hidden, const void* weight, int D, int V,
+                         const fb_pack* pack, void* lm_ws, const LmSizes& z, void* upd_ws,
+                         const UpdateSizes& uz, hipStream_t stream) {
+    PackView pv = pack_view(pack);
+    float4* lm_part = static_cast<float4*>(lm_ws);
+    hipLaunchKernelGGL(lmhead_kernel, dim3((unsigned)(z.n_rtiles * z.P)), dim3(kLmThreads), 0,
+                       stream, static_cast<const uint16_t*>(hidden),
+                       static_cast<const uint16_t*>(weight), D, V, pack->row_cap, z.n_rtiles,
+                       z.n_vtiles, z.tiles_per_part, z.P, pv, lm_part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int rows_per_wg = kMergeThreads / 64;
+    hipLaunchKernelGGL(lm_merge_kernel,
+                       dim3((unsigned)((pack->row_cap + rows_per_wg - 1) / rows_per_wg)),
+                       dim3(kMergeThreads), 0, stream, lm_part, z.P, pv, pack->row_cap,
+                       static_cast<float4*>(upd_ws), uz.nsplit);
+    return hipGetLastError();
+}
+
+}  // namespace fb

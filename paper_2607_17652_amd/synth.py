@@ -357,3 +357,35 @@ def make_loop_host_state(B, prompts, n_blocks, bl, V, page_size, seed=0):
                 fin=np.zeros((B, n_blocks), dtype=np.int64),
                 page_table=page_table, num_pages=num_pages, T_max=T_max,
                 n_max=n_blocks, max_pages=max_pages)
+
+
+# ----------------------------------------------------------- LM head ------
+def make_lmhead_tensors(wl, D, seed=0, device="cuda", planted=None):
+    """Hidden rows [row_cap, D] and an LM-head weight [V, D], bf16, whose
+    product has the logit statistics of the workload: weight rows ~ N(0, 1/D)
+    (norm about 1), hidden rows sigma_row * N(0, 1) with sigma_row ~ U[sigma],
+    so a row's logits are about N(0, sigma_row^2); on a seeded fraction of rows
+    (the workload's planted share) the hidden row also gets a component along
+    one weight row that lifts that logit about 4 above the row's maximum."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed) * 7919 + 13)
+    V, cap = wl.V, wl.row_cap
+    weight = torch.empty((V, D), dtype=torch.bfloat16, device=device)
+    for v0 in range(0, V, 16384):
+        v1 = min(V, v0 + 16384)
+        weight[v0:v1] = (torch.randn((v1 - v0, D), generator=gen, device=device)
+                         / np.sqrt(D)).to(torch.bfloat16)
+    lo, hi = wl.sigma
+    sig = lo + (hi - lo) * torch.rand((cap, 1), generator=gen, device=device)
+    hid = torch.randn((cap, D), generator=gen, device=device) * sig
+    frac = wl.planted if planted is None else planted
+    plant = torch.rand((cap,), generator=gen, device=device) < frac
+    k = torch.randint(0, V - 1, (cap,), generator=gen, device=device)
+    idx = torch.nonzero(plant).flatten()
+    if len(idx):
+        wk = weight[k[idx]].float()
+        # the maximum of V Gaussian logits is about sigma * sqrt(2 ln V)
+        lift = sig[idx, 0] * float(np.sqrt(2 * np.log(V))) + 4.0
+        hid[idx] += wk * (lift / (wk * wk).sum(dim=1))[:, None]
+    return hid.to(torch.bfloat16), weight

@@ -241,3 +241,55 @@ def test_synchronous_admission_uses_the_minimum_readiness(theta, admitted):
     hwp = _one_step(st, tok, z, z, logits, prm)
     assert hwp["state"]["R"][0] == 3
     assert hwp["state"]["R"][1] == (3 if admitted else 2)
+
+
+# ---- LM head with the fused vocabulary reduction ---------------------------
+def test_lmhead_reduce_is_the_reduction_of_the_product():
+    from oracle import lmhead
+    rng = np.random.default_rng(4)
+    H = rng.standard_normal((5, 16))
+    Wt = rng.standard_normal((37, 16))
+    xh, p = lmhead.lmhead_reduce(H, Wt)
+    Z = np.array([[sum(H[r, i] * Wt[v, i] for i in range(16)) for v in range(37)]
+                  for r in range(5)])                  # the product, written out
+    for r in range(5):
+        assert xh[r] == int(np.argmax(Z[r]))
+        assert abs(p[r] - 1.0 / math.fsum(math.exp(z - Z[r].max()) for z in Z[r])) < 1e-14
+
+
+def test_lmhead_identity_weight_reduces_the_hidden_rows():
+    """W = I (V = D): the logits are the hidden rows themselves."""
+    from oracle import lmhead
+    rng = np.random.default_rng(5)
+    H = rng.standard_normal((4, 12))
+    xh, p = lmhead.lmhead_reduce(H, np.eye(12))
+    x2, p2 = update.vocab_reduce(H)
+    assert np.array_equal(xh, x2) and np.allclose(p, p2, rtol=0, atol=1e-15)
+
+
+def test_lmhead_two_level_closed_form():
+    """One hidden direction picked out by one weight row: z = a at k, 0
+    elsewhere, p = e^a / (e^a + V - 1); a weight of a non-square shape
+    catches a transposed operand."""
+    from oracle import lmhead
+    V, D, k, a = 50, 8, 17, 3.0
+    H = np.zeros((1, D))
+    H[0, 2] = a
+    Wt = np.zeros((V, D))
+    Wt[k, 2] = 1.0
+    xh, p = lmhead.lmhead_reduce(H, Wt)
+    assert xh[0] == k
+    assert abs(p[0] - math.exp(a) / (math.exp(a) + V - 1)) < 1e-15
+
+
+def test_lmhead_accumulation_bound_covers_float32_products():
+    from oracle import lmhead
+    rng = np.random.default_rng(6)
+    H = rng.standard_normal((6, 512)).astype(np.float32)
+    Wt = rng.standard_normal((40, 512)).astype(np.float32)
+    exact = lmhead.lm_logits(H, Wt)
+    f32 = np.zeros((6, 40), dtype=np.float32)
+    for i in range(512):                       # sequential float32 accumulation
+        f32 = (f32 + np.outer(H[:, i], Wt[:, i]).astype(np.float32)).astype(np.float32)
+    bound = lmhead.accumulation_bound(H, Wt)
+    assert np.all(np.abs(f32 - exact).max(axis=1) <= bound)

@@ -50,6 +50,11 @@ MUTATIONS = [
      "staleness counts the block's own masks"),
     ("synth_model.py", "lvl = 3 if p == first else (h >> 32) % 4",
      "lvl = (h >> 32) % 4", "no guaranteed reveal per forward"),
+    ("lmhead.py", "@ np.asarray(weight, dtype=np.float64).T",
+     "@ np.asarray(weight, dtype=np.float64)[:, :hidden.shape[0]]",
+     "LM head takes the wrong operand orientation"),
+    ("lmhead.py", "gamma = D * u / (1.0 - D * u)", "gamma = u",
+     "accumulation bound without the length factor"),
 ]
 
 
