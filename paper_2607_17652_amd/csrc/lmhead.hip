@@ -71,19 +71,21 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
 
     // ---- DMA assignment: wave w fills W rows [32w, 32w+32) and H rows
     // [32w, 32w+32) of each stage, 8 rows (1 KB) per instruction; lane L
-    // writes LDS chunk L%8 of row L/8, which holds logical K chunk
-    // (L%8) ^ (row%8) -- the swizzle that makes the operand reads
-    // conflict-free.
+    // writes LDS chunk L%8 of row r = 32w + 8j + L/8, which holds logical K
+    // chunk (L%8) ^ ((r/2)%8).  With 128-byte rows, 16 consecutive rows then
+    // cover all 16 bank groups of 16 bytes at any logical chunk, so the
+    // operand reads (16 lanes = 16 rows per access) are conflict-free.
     const int lrow = lane >> 3;
-    const int lchunk = (lane & 7) ^ lrow;            // row % 8 == lrow
     uint32_t h_off[4];
-    int w_row[4];
+    int w_row[4], w_chunk[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int r = wave * 32 + j * 8 + lrow;
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
         const int tr = min(row0 + r, row_cap - 1);
-        h_off[j] = (uint32_t)(((size_t)tr * D + lchunk * 8) * 2);
+        h_off[j] = (uint32_t)(((size_t)tr * D + c * 8) * 2);
         w_row[j] = r;
+        w_chunk[j] = c;
     }
     uint32_t m0_w[4], m0_h[4];
     const uint32_t lds_base = (uint32_t)(uintptr_t)&lds[0];
@@ -97,14 +99,13 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int vr = min(vt * kTileV + w_row[j], V - 1);
-            w_off[j] = (uint32_t)(((size_t)vr * D + lchunk * 8) * 2);
+            w_off[j] = (uint32_t)(((size_t)vr * D + w_chunk[j] * 8) * 2);
         }
     };
     const int KS = D / kBK;
-    const int n_it = (vt1 - vt0) * KS;
-    // issue iteration `it` (vocabulary tile vt0 + it/KS, K step it%KS) into `stage`
-    auto issue = [&](int it, int stage) {
-        const int k0 = (it % KS) * kBK;
+    // issue K step ks of the current DMA tile into `stage`
+    auto issue = [&](int ks, int stage) {
+        const int k0 = ks * kBK;
         const uint16_t* wb = W + k0;
         const uint16_t* hb = H + k0;
         const uint32_t so = stage * kStageBytes;
@@ -118,8 +119,9 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
                          :: "s"(m0_h[j] + so), "v"(h_off[j]), "s"(hb) : "memory");
     };
 
-    // operand reads: row r of a stage part, logical chunk 2kk + h
-    const uint32_t swz = (uint32_t)((h ^ (n & 7)) * 16);
+    // operand reads: row r of a stage part, logical chunk 2kk + h, stored at
+    // chunk (2kk + h) ^ ((r/2)%8); every row read here has (r/2)%8 == (n/2)%8
+    const uint32_t swz = (uint32_t)((h ^ ((n >> 1) & 7)) * 16);
     const uint32_t a_row = (uint32_t)((wv * 128 + n) * kRowBytes);
     const uint32_t b_row = (uint32_t)(kHalfBytes + (wt * 64 + n) * kRowBytes);
 
@@ -155,7 +157,7 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
     // is vocabulary id vt*256 + wv*128 + vi*32 + (r/4)*8 + h*4 + r%4 --
     // increasing in (vi, r), so the first maximum in that order is the
     // lowest id.
-    auto fold = [&](int vt) {
+    auto fold = [&](int vt, auto partial) {
         const int vbase = vt * kTileV + wv * 128 + h * 4;
 #pragma unroll
         for (int ti = 0; ti < 2; ++ti) {
@@ -165,7 +167,7 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int v = vbase + vi * 32 + (r >> 2) * 8 + (r & 3);
-                    f[vi * 16 + r] = v < V ? acc[vi][ti][r] : -INFINITY;
+                    f[vi * 16 + r] = (!partial || v < V) ? acc[vi][ti][r] : -INFINITY;
                 }
             float vmax = f[0];
 #pragma unroll
@@ -197,19 +199,35 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
             for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
     };
 
-    // ---- main loop: double-buffered stages over the flattened (tile, K step)
+    // ---- main loop: double-buffered stages; the loads run one K step
+    // ahead, across tile boundaries
     set_vtile(vt0);
     issue(0, 0);
-    for (int it = 0; it < n_it; ++it) {
-        const int stage = it & 1;
-        wait_vm0();
-        lds_barrier();             // stage `it` landed; stage it-1 is free
-        if (it + 1 < n_it) {
-            if ((it + 1) % KS == 0) set_vtile(vt0 + (it + 1) / KS);
-            issue(it + 1, stage ^ 1);
+    int nvt = vt0, nks = 1;        // next K step to load
+    if (nks == KS) {
+        nvt += 1;
+        nks = 0;
+        if (nvt < vt1) set_vtile(nvt);
+    }
+    int stage = 0;
+    for (int vt = vt0; vt < vt1; ++vt) {
+        for (int ks = 0; ks < KS; ++ks) {
+            wait_vm0();
+            lds_barrier();         // this step's stage landed; the other is free
+            if (nvt < vt1) {
+                issue(nks, stage ^ 1);
+                if (++nks == KS) {
+                    nks = 0;
+                    if (++nvt < vt1) set_vtile(nvt);
+                }
+            }
+            compute(stage);
+            stage ^= 1;
         }
-        compute(stage);
-        if (it % KS == KS - 1) fold(vt0 + it / KS);
+        if ((vt + 1) * kTileV > V)
+            fold(vt, std::true_type{});
+        else
+            fold(vt, std::false_type{});
     }
 
     // ---- merge: lane halves, then the two vocabulary halves of each token
