@@ -46,6 +46,10 @@ def parse_args():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-loop", action="store_true",
                     help="skip the whole-decode loop runs on the synthetic model")
+    ap.add_argument("--no-lmhead", action="store_true",
+                    help="skip the LM head with the fused vocabulary reduction")
+    ap.add_argument("--lmhead-dim", type=int, default=2048,
+                    help="hidden size D of the LM-head measurement")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -230,6 +234,52 @@ def graph_replay(torch, fb, step, one_step, copies, K, W):
             "steps_per_replay": K}
 
 
+def lmhead_bench(torch, fb, synth, wl, step, logits, n_live, D, reps=5):
+    """The LM head Z = H W^T of the workload's live rows with the vocabulary
+    reduction as its epilogue (fb_lmhead_reduce), against the unfused path:
+    the library GEMM of torch (hipBLASLt) writing bf16 logits, then
+    fb_vocab_reduce reading them."""
+    hid, weight = synth.make_lmhead_tensors(wl, D, seed=1)
+    lm_ws = torch.empty(fb.fb_lmhead_workspace_bytes(step.pack, wl.V, D), dtype=torch.uint8,
+                        device="cuda")
+    flops = 2.0 * n_live * wl.V * D
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for _ in range(2):
+        fb.fb_lmhead_reduce(hid, weight, step.pack, lm_ws, step.upd_ws)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        fb.fb_lmhead_reduce(hid, weight, step.pack, lm_ws, step.upd_ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    fused_ms = ev[0].elapsed_time(ev[1]) / reps
+    rows = hid[:n_live] if wl.layout == "ragged" else hid
+    out = logits[:rows.shape[0]]
+    for _ in range(2):
+        torch.matmul(rows, weight.t(), out=out)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        torch.matmul(rows, weight.t(), out=out)
+    ev[1].record()
+    for _ in range(reps):
+        fb.fb_vocab_reduce(logits, step.pack, step.upd_ws)
+    ev[2].record()
+    torch.cuda.synchronize()
+    gemm_ms = ev[0].elapsed_time(ev[1]) / reps
+    vp_ms = ev[1].elapsed_time(ev[2]) / reps
+    achieved = flops / (fused_ms * 1e-3)
+    return {"kernel": "lmhead_kernel + lm_merge_kernel", "D": D, "V": wl.V, "rows": n_live,
+            "flops": flops, "ms": fused_ms,
+            "roofline": {"bound": "mfma", "achieved": achieved / 1e12,
+                         "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
+                         "frac": achieved / PEAK_BF16_FLOPS},
+            "unfused": {"gemm_ms": gemm_ms, "gemm_tflops": flops / (gemm_ms * 1e-3) / 1e12,
+                        "vocab_reduce_ms": vp_ms, "total_ms": gemm_ms + vp_ms,
+                        "logit_bytes_written_and_read": 2.0 * n_live * wl.V * 2},
+            "fused_over_unfused": (gemm_ms + vp_ms) / fused_ms}
+
+
 LOOP_WORKLOAD = dict(name="loop64", B=64, prompt=(256, 1024), n_blocks=16, bl=32,
                      W_max=4, V=157184, Hq=32, Hkv=8, d=128, seed=0)
 
@@ -402,14 +452,19 @@ def main():
     }
     if graph is not None:
         out["graph"] = graph
-    if not args.no_loop:
-        del copies
-        out["loop"] = loop_bench(torch, fb, synth, DecodeLoop)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
         cb["cpu_model"] = cpu_model()
         out["cpu_baseline"] = cb
+    # the sections below reuse the step's buffers (the LM head overwrites its
+    # logits), so they run after everything that reads the step's inputs
+    if not args.no_lmhead:
+        out["lmhead"] = lmhead_bench(torch, fb, synth, wl, step, t["logits"], n_live,
+                                     args.lmhead_dim)
+    if not args.no_loop:
+        del copies
+        out["loop"] = loop_bench(torch, fb, synth, DecodeLoop)
     print(json.dumps(out), flush=True)
 
 
