@@ -157,3 +157,68 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     bad = fb.fb_pack()
     rc = lib.fb_pack_wavefronts(fake, None, 4, 64, ctypes.byref(bad), None)
     assert rc == fb.FB_E_INVAL
+
+
+def test_loop_and_lmhead_calls_reject_bad_arguments_before_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10004)
+    rc, h = _init(lib, fake, fb.fb_pack_bytes(2, 2, 32), 2, 2, 32, fb.FB_RAGGED)
+    assert rc == fb.FB_OK
+    P = ctypes.byref(h)
+    # LM head: D a multiple of 64, sizes, pointers, alignment, workspaces
+    assert lib.fb_lmhead_workspace_bytes(P, 1000, 100) == 0
+    assert lib.fb_lmhead_workspace_bytes(P, 1000, 128) > 0
+    big = 1 << 30
+    assert lib.fb_lmhead_reduce(fake, fake, 100, 1000, P, fake, big, fake, big,
+                                None) == fb.FB_E_UNSUPPORTED
+    assert lib.fb_lmhead_reduce(fake, fake, 1 << 14, 1 << 17, P, fake, big, fake, big,
+                                None) == fb.FB_E_UNSUPPORTED
+    assert lib.fb_lmhead_reduce(None, fake, 128, 1000, P, fake, big, fake, big,
+                                None) == fb.FB_E_INVAL
+    assert lib.fb_lmhead_reduce(odd, fake, 128, 1000, P, fake, big, fake, big,
+                                None) == fb.FB_E_INVAL
+    assert lib.fb_lmhead_reduce(fake, fake, 128, 1000, P, fake, 16, fake, big,
+                                None) == fb.FB_E_WORKSPACE
+    assert lib.fb_lmhead_reduce(fake, fake, 128, 1000, P, fake, big, fake, 16,
+                                None) == fb.FB_E_WORKSPACE
+    # synthetic model: levels positive, finite and exact in the logits dtype
+    st = fake
+    m = fb.make_model(1, (6.0, 8.625, 10.0, 11.5))
+    assert lib.fb_synth_logits(st, fake, 64, P, ctypes.byref(m), 1000, fb.FB_BF16,
+                               odd, fake, None) == fb.FB_E_INVAL          # pred alignment
+    assert lib.fb_synth_logits(st, fake, 64, P, ctypes.byref(m), 1, fb.FB_BF16,
+                               fake, fake, None) == fb.FB_E_INVAL         # V < 2
+    m2 = fb.make_model(1, (6.0, 8.6, 10.0, 11.5))                       # 8.6 not bf16
+    assert lib.fb_synth_logits(st, fake, 64, P, ctypes.byref(m2), 1000, fb.FB_BF16,
+                               fake, fake, None) == fb.FB_E_INVAL
+    assert "bf16" in fb.fb_last_error()
+    m3 = fb.make_model(1, (0.0, 8.625, 10.0, 11.5))
+    assert lib.fb_synth_logits(st, fake, 64, P, ctypes.byref(m3), 1000, fb.FB_F32,
+                               fake, fake, None) == fb.FB_E_INVAL
+    sh = fb.make_shape(8, 4, 96, fb.FB_BF16, 32, 4, 8)
+    assert lib.fb_synth_embed(P, ctypes.byref(sh), 1, fake, fake, fake,
+                              None) == fb.FB_E_UNSUPPORTED
+    # decode loop
+    prm = fb.make_params(0.9, 0.8, 0.5, 999, -1, 2, 2)
+    a = fb.fb_loop_args()
+    a.st = a.tokens = a.pe = a.fin = a.logits = a.pred = a.conf = a.argmax = 0x10000
+    a.T_max, a.n_max, a.V, a.logit_dtype = 64, 4, 1000, fb.FB_BF16
+    a.pack = ctypes.pointer(h)
+    a.prm = ctypes.pointer(prm)
+    a.model = ctypes.pointer(m)
+    a.upd_ws, a.upd_ws_bytes = 0x10000, big
+    a.counters = a.forwards = 0x10000
+    steps, done = ctypes.c_int(-1), ctypes.c_int(-1)
+    call = lambda *x: lib.fb_decode_loop(ctypes.byref(a), *x, ctypes.byref(steps),
+                                         ctypes.byref(done), None)
+    assert call(10, 0, 0) == fb.FB_E_INVAL                      # check_every 0
+    assert call(10, 4, 1) == fb.FB_E_INVAL                      # graph on the null stream
+    prm.mask_id = 5
+    assert call(10, 4, 0) == fb.FB_E_INVAL                      # mask_id != V - 1
+    prm.mask_id = 999
+    a.counters = 0
+    assert call(10, 4, 0) == fb.FB_E_INVAL
+    a.counters = 0x10000
+    a.upd_ws_bytes = 16
+    assert call(10, 4, 0) == fb.FB_E_WORKSPACE
+    assert steps.value == -1 and done.value == -1               # nothing ran
