@@ -1,11 +1,11 @@
 // Window KV write-back, Eq. 6 (Sec. 4.2, "KV retrieval and write-back"):
 // the fresh K/V of each live block lands at its absolute positions of the
 // paged caches.  One workgroup per (tile, KV head).  K rows are copied in
-// 16-byte vectors.  V is written key-innermost ([page][head][d][slot]): when
-// the block starts on a 16-byte slot boundary each thread gathers one
-// 16-byte run of slots for one d and stores it whole (neighbouring lanes
-// fill neighbouring runs of the same d row); otherwise V is staged through
-// LDS and stored element by element.
+// 16-byte vectors.  V is written key-innermost ([page][head][d][slot]): the
+// block's V rows are staged in LDS with 16-byte loads; when the block starts
+// on a 16-byte slot boundary each thread then gathers one 16-byte run of
+// slots for one d from LDS and stores it whole (neighbouring lanes fill
+// neighbouring runs of the same d row), otherwise element by element.
 #include "internal.h"
 
 namespace fb {
@@ -18,9 +18,9 @@ __global__ void __launch_bounds__(kKvThreads)
 write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
                 T* __restrict__ k_cache, T* __restrict__ v_cache,
                 const int32_t* __restrict__ page_table, PackView pv, int Hkv,
-                int D, int bl, int ps, int max_pages, int num_pages) {
+                int D, int bl, int ps, int max_pages, int num_pages, int pitch) {
     extern __shared__ unsigned char kv_smem[];
-    T* vs = reinterpret_cast<T*>(kv_smem);   // [bl][D]
+    T* vs = reinterpret_cast<T*>(kv_smem);   // [bl][pitch]
     const int t = blockIdx.x;
     const int c = blockIdx.y;
     if (t >= pv.hdr[kHdrTiles]) return;
@@ -49,9 +49,19 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
         *reinterpret_cast<uint4*>(k_cache + dst) =
             *reinterpret_cast<const uint4*>(k_new + src);
     }
+    // V: stage the block's V rows in LDS ([bl][pitch], 16-byte loads), then
+    // write the cache's key-innermost rows.
+    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
+        const int i = e / dch;
+        const int dc = e % dch;
+        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
+        *reinterpret_cast<uint4*>(vs + (size_t)i * pitch + dc * VEC) =
+            *reinterpret_cast<const uint4*>(v_new + src);
+    }
+    __syncthreads();
     if (pos0 % VEC == 0 && ps % VEC == 0 && bl % VEC == 0) {
-        // V: run ic of VEC slots for dimension d; lanes walk the runs of a d
-        // row first, so a wave stores whole d rows of the page.
+        // run ic of VEC slots for dimension d, gathered from LDS; lanes walk
+        // the runs of a d row first, so a wave stores whole d rows of a page
         const int nrun = bl / VEC;
         for (int e = threadIdx.x; e < D * nrun; e += kKvThreads) {
             const int ic = e % nrun;
@@ -65,21 +75,12 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
                 T x[VEC];
             } run;
 #pragma unroll
-            for (int k = 0; k < VEC; ++k)
-                run.x[k] = v_new[((size_t)(row0 + ic * VEC + k) * Hkv + c) * D + d];
+            for (int k = 0; k < VEC; ++k) run.x[k] = vs[(size_t)(ic * VEC + k) * pitch + d];
             *reinterpret_cast<uint4*>(v_cache + (((size_t)page * Hkv + c) * D + d) * ps +
                                       (pos % ps)) = run.v;
         }
         return;
     }
-    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
-        const int i = e / dch;
-        const int dc = e % dch;
-        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
-        *reinterpret_cast<uint4*>(vs + (size_t)i * D + dc * VEC) =
-            *reinterpret_cast<const uint4*>(v_new + src);
-    }
-    __syncthreads();
     for (int e = threadIdx.x; e < bl * D; e += kKvThreads) {
         const int d = e / bl;
         const int i = e % bl;
@@ -88,7 +89,7 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
         const int page = pidx < max_pages ? pt[pidx] : -1;
         if (page < 0 || page >= num_pages) continue;
         v_cache[(((size_t)page * Hkv + c) * D + d) * ps + (pos % ps)] =
-            vs[(size_t)i * D + d];
+            vs[(size_t)i * pitch + d];
     }
 }
 
@@ -100,24 +101,29 @@ hipError_t launch_write_kv(const void* k_new, const void* v_new, void* k_cache,
                            hipStream_t stream) {
     PackView pv = pack_view(pack);
     const dim3 grid(pack->tile_cap, sh->Hkv);
+    // LDS rows padded by 16 bytes (when that still fits 64 KB) so the
+    // column gathers of neighbouring rows fall in different banks
+    const size_t elt = sh->dtype == FB_BF16 ? 2 : 4;
+    int pitch = sh->head_dim + (int)(16 / elt);
+    if ((size_t)pack->bl * pitch * elt > 65536) pitch = sh->head_dim;
     if (sh->dtype == FB_BF16) {
-        const size_t smem = (size_t)pack->bl * sh->head_dim * 2;
+        const size_t smem = (size_t)pack->bl * pitch * 2;
         hipLaunchKernelGGL(write_kv_kernel<uint16_t>, grid, dim3(kKvThreads),
                            smem, stream, static_cast<const uint16_t*>(k_new),
                            static_cast<const uint16_t*>(v_new),
                            static_cast<uint16_t*>(k_cache),
                            static_cast<uint16_t*>(v_cache), page_table, pv,
                            sh->Hkv, sh->head_dim, pack->bl, sh->page_size,
-                           sh->max_pages, sh->num_pages);
+                           sh->max_pages, sh->num_pages, pitch);
     } else {
-        const size_t smem = (size_t)pack->bl * sh->head_dim * 4;
+        const size_t smem = (size_t)pack->bl * pitch * 4;
         hipLaunchKernelGGL(write_kv_kernel<float>, grid, dim3(kKvThreads), smem,
                            stream, static_cast<const float*>(k_new),
                            static_cast<const float*>(v_new),
                            static_cast<float*>(k_cache),
                            static_cast<float*>(v_cache), page_table, pv, sh->Hkv,
                            sh->head_dim, pack->bl, sh->page_size, sh->max_pages,
-                           sh->num_pages);
+                           sh->num_pages, pitch);
     }
     return hipGetLastError();
 }
