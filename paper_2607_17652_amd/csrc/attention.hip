@@ -393,6 +393,9 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const size_t k_head = (size_t)c * ps * D;        // head c inside a K page
     const size_t v_head = (size_t)c * D * ps;        // head c inside a V page
     const size_t page_elems = (size_t)Hkv * ps * D;  // one page of one cache
+    const uint32_t page_bytes = (uint32_t)(page_elems * 2);
+    const unsigned char* kb0 = reinterpret_cast<const unsigned char*>(k_cache + k_head);
+    const unsigned char* vb0 = reinterpret_cast<const unsigned char*>(v_cache + v_head);
 
     // Per-lane LDS byte offsets of the MFMA operand reads (stage 0).
     const int krow = swap_bits23(n);
@@ -421,16 +424,20 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         const int key0 = kt * kKeyTile;
         if (FAST) {
             // one page per tile: uniform base + per-lane constant offsets
-            const bool okp = page >= 0 && page < num_pages;
+            const bool okp = (unsigned)page < (unsigned)num_pages;
             page_err |= !okp;
             page = okp ? page : 0;
-            const size_t inpage = (size_t)(key0 & (ps - 1));
-            const uint16_t* kbase = k_cache + (size_t)page * page_elems + k_head + inpage * D;
-            const uint16_t* vbase = v_cache + (size_t)page * page_elems + v_head + inpage;
+            const uint32_t inpage = (uint32_t)(key0 & (ps - 1));
+            const size_t poff = (size_t)(uint32_t)page * (size_t)page_bytes;
+            const unsigned char* kbase = kb0 + poff + inpage * (uint32_t)(D * 2);
+            const unsigned char* vbase = vb0 + poff + inpage * 2u;
 #pragma unroll
             for (int j = 0; j < NCH; ++j) {
                 const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
-                const uint16_t* base = ld_isk[j] ? kbase : vbase;
+                // for D >= 64 the K chunks are exactly the first kKCh/256 loads
+                const bool isk = (RG_::kKCh % kAttnThreads == 0) ? (j * kAttnThreads < RG_::kKCh)
+                                                                 : ld_isk[j];
+                const unsigned char* base = isk ? kbase : vbase;
                 asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                              :: "s"(m0), "v"(ch_off[j]), "s"(base) : "memory");
             }
@@ -475,6 +482,16 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = floatx16{};
     float m_run = -INFINITY;   // running max of scores, log2 domain
+    float thr_raw = -INFINITY;  // raw score above which the running max moves
+    // max over the two lane halves (rows are shared by lanes l and l+32);
+    // plain v_max_f32 on values that are never NaN here
+    auto half_max = [&](float mx) -> float {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        float r;
+        asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(__uint_as_float(sw[0])), "v"(__uint_as_float(sw[1])));
+        return r;
+    };
     float l_acc[2] = {0.f, 0.f};   // this lane's share of the denominator
     bf16x8 pb[2];              // P^T of the current tile (B operand of PV)
 
@@ -520,9 +537,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
         for (int x = 3; x < 16; x += 2) mx = fmaxf(fmaxf(mx, s[x]), x + 1 < 16 ? s[x + 1] : s[x]);
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
-                                                         false, false);
-        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+        return half_max(mx) * scale_log2;
     };
     // P^T = exp2(S^T * scale - m) rounded to bf16, and the denominator from
     // the same rounded weights the PV product uses.
@@ -550,10 +565,11 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     };
     // Lazy rescale: move the running max only when a row's tile max passes
     // it by more than the slack; O and the denominator follow.
+    // mx is a raw row max (not scaled); rescale when it passes thr_raw
     auto update_max = [&](float mx) {
-        const bool need = mx > m_run + kRescaleSlack;
+        const bool need = mx > thr_raw;
         if (__any(need)) {
-            const float m_new = need ? mx : m_run;
+            const float m_new = need ? mx * scale_log2 : m_run;
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt)
@@ -562,6 +578,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             l_acc[0] *= alpha;
             l_acc[1] *= alpha;
             m_run = m_new;
+            thr_raw = (m_run + kRescaleSlack) / scale_log2;
         }
     };
 
@@ -619,9 +636,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             for (int y = 0; y < VPG; ++y) mx = fmaxf(mx, sn[x * VPG + y]);
             __builtin_amdgcn_sched_barrier(0);
         }
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
-                                                         false, false);
-        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+        return half_max(mx);
     };
 
     // Software pipeline over key tiles, one step per tile i < nt-1:
@@ -684,6 +699,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         s_mfmas(ring, s_cur);
         if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
         m_run = tile_max(s_cur);
+        thr_raw = (m_run + kRescaleSlack) / scale_log2;
         using Full = std::integral_constant<int, 0>;
         using Near = std::integral_constant<int, 1>;
         using Last = std::integral_constant<int, 2>;
