@@ -234,6 +234,32 @@ def graph_replay(torch, fb, step, one_step, copies, K, W):
             "steps_per_replay": K}
 
 
+def prologue_bench(torch, fb, step, t, reps=20):
+    """The window prologue (RoPE on the live rows' Q and K at absolute
+    positions + the Eq. 6 write) against the plain window KV write it
+    replaces, on the step's own inputs (it rewrites the window part of the
+    caches, which the step rewrites anyway)."""
+    q_out = torch.empty_like(t["q"])
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for _ in range(2):
+        fb.fb_window_prologue(t["q"], q_out, t["k_new"], t["v_new"], t["k_cache"],
+                              t["v_cache"], step.page_table, step.pack, step.shape)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        fb.fb_window_prologue(t["q"], q_out, t["k_new"], t["v_new"], t["k_cache"],
+                              t["v_cache"], step.page_table, step.pack, step.shape)
+    ev[1].record()
+    for _ in range(reps):
+        fb.fb_write_window_kv(t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                              step.page_table, step.pack, step.shape)
+    ev[2].record()
+    torch.cuda.synchronize()
+    return {"kernel": "rope_kv_kernel", "rope_base": 10000.0,
+            "ms": ev[0].elapsed_time(ev[1]) / reps,
+            "kv_write_only_ms": ev[1].elapsed_time(ev[2]) / reps}
+
+
 def lmhead_bench(torch, fb, synth, wl, step, logits, n_live, D, reps=5):
     """The LM head Z = H W^T of the workload's live rows with the vocabulary
     reduction as its epilogue (fb_lmhead_reduce), against the unfused path:
@@ -459,6 +485,7 @@ def main():
         out["cpu_baseline"] = cb
     # the sections below reuse the step's buffers (the LM head overwrites its
     # logits), so they run after everything that reads the step's inputs
+    out["prologue"] = prologue_bench(torch, fb, step, t)
     if not args.no_lmhead:
         out["lmhead"] = lmhead_bench(torch, fb, synth, wl, step, t["logits"], n_live,
                                      args.lmhead_dim)

@@ -238,6 +238,25 @@ int fb_write_window_kv(const void* k_new, const void* v_new, void* k_cache,
                        const fb_pack* pack, const fb_attn_shape* sh,
                        void* stream);
 
+/* Window prologue: rotary position embedding (RoPE, rotate-half
+ * arrangement) at the rows' absolute positions -- the absolute RoPE position
+ * ids of Sec. 4.2 (Fig. 2b) -- on the live rows' queries and fresh keys,
+ * fused with the Eq. 6 write above: keys are rotated on their way into the
+ * K cache, values written as fb_write_window_kv writes them.  Pair j of a
+ * head vector, (x_j, x_{j+d/2}), turns by the angle p * rope_base^(-2j/d)
+ * (angles in float64, products in float32, results rounded to the dtype).
+ * Use it in place of fb_write_window_kv when the model hands over Q/K before
+ * RoPE; the attention then reads q_out.
+ *   q_in, q_out   [row_cap][Hq][d]; may be the same buffer (in place); rows
+ *                 that are not live are not written
+ *   k_new, v_new, caches, page_table  as for fb_write_window_kv
+ *   rope_base     > 1 (10000 in the original RoPE)
+ * Needs bl * d * 4 <= 65536 (the block's cos/sin table lives in LDS). */
+int fb_window_prologue(const void* q_in, void* q_out, const void* k_new,
+                       const void* v_new, void* k_cache, void* v_cache,
+                       const int32_t* page_table, const fb_pack* pack,
+                       const fb_attn_shape* sh, double rope_base, void* stream);
+
 /* ---- Sec. 4.1 / Eq. 5: block-causal window attention ------------------- */
 
 /* Workspace bytes for fb_wavefront_attention with this pack and shape. */

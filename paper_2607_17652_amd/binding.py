@@ -42,7 +42,7 @@ EXPORTS = [
     "fb_wavefront_attention", "fb_update_workspace_bytes", "fb_denoise_update",
     "fb_vocab_reduce", "fb_denoise_apply",
     "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
-    "fb_lmhead_workspace_bytes", "fb_lmhead_reduce",
+    "fb_lmhead_workspace_bytes", "fb_lmhead_reduce", "fb_window_prologue",
 ]
 
 
@@ -145,6 +145,8 @@ def lib():
             "fb_denoise_apply": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, i32,
                                        P(fb_pack), P(fb_update_params), vp, vp, sz,
                                        vp]),
+            "fb_window_prologue": (i32, [vp, vp, vp, vp, vp, vp, vp, P(fb_pack),
+                                         P(fb_attn_shape), ctypes.c_double, vp]),
             "fb_lmhead_workspace_bytes": (sz, [P(fb_pack), i32, i32]),
             "fb_lmhead_reduce": (i32, [vp, vp, i32, i32, P(fb_pack), vp, sz, vp, sz, vp]),
             "fb_synth_embed": (i32, [P(fb_pack), P(fb_attn_shape), ctypes.c_uint64,
@@ -283,6 +285,13 @@ def fb_write_window_kv(k_new, v_new, k_cache, v_cache, page_table, pack, shape,
     _check(lib().fb_write_window_kv(_ptr(k_new), _ptr(v_new), _ptr(k_cache),
                                     _ptr(v_cache), _ptr(page_table), pack.ref(),
                                     ctypes.byref(shape), _stream(stream)))
+
+
+def fb_window_prologue(q_in, q_out, k_new, v_new, k_cache, v_cache, page_table, pack, shape,
+                       rope_base=10000.0, stream=None):
+    _check(lib().fb_window_prologue(_ptr(q_in), _ptr(q_out), _ptr(k_new), _ptr(v_new),
+                                    _ptr(k_cache), _ptr(v_cache), _ptr(page_table), pack.ref(),
+                                    ctypes.byref(shape), float(rope_base), _stream(stream)))
 
 
 def fb_attention_workspace_bytes(pack, shape):

@@ -188,6 +188,30 @@ int fb_write_window_kv(const void* k_new, const void* v_new, void* k_cache, void
     return ok();
 }
 
+int fb_window_prologue(const void* q_in, void* q_out, const void* k_new, const void* v_new,
+                       void* k_cache, void* v_cache, const int32_t* page_table,
+                       const fb_pack* pack, const fb_attn_shape* sh, double rope_base,
+                       void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_shape(pack, sh);
+    if (rc) return rc;
+    if (!q_in || !q_out || !k_new || !v_new || !k_cache || !v_cache || !page_table)
+        return fail(FB_E_INVAL, "a tensor pointer is NULL");
+    if (!aligned16(q_in) || !aligned16(q_out) || !aligned16(k_new) || !aligned16(v_new) ||
+        !aligned16(k_cache) || !aligned16(v_cache))
+        return fail(FB_E_INVAL, "q, K/V pointers must be 16-byte aligned");
+    if (!(rope_base > 1.0) || isinf(rope_base))
+        return fail(FB_E_INVAL, "rope_base must be finite and > 1");
+    if ((size_t)pack->bl * sh->head_dim * 4 > 65536)
+        return fail(FB_E_UNSUPPORTED, "bl*head_dim too large for the block's cos/sin table");
+    hipError_t e = fb::launch_window_prologue(q_in, q_out, k_new, v_new, k_cache, v_cache,
+                                              page_table, pack, sh, rope_base,
+                                              (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "window prologue launch");
+    return ok();
+}
+
 size_t fb_attention_workspace_bytes(const fb_pack* pack, const fb_attn_shape* sh) {
     if (check_pack(pack) || check_shape(pack, sh)) return 0;
     return fb::attention_sizes(pack, sh, cu_count()).total;

@@ -93,6 +93,13 @@ hipError_t launch_apply(int32_t* tokens, int T_max, float* conf, int32_t* argmax
                         fb_req_stats* stats, const void* ws, const UpdateSizes& sz,
                         hipStream_t stream);
 
+size_t prologue_smem_bytes(const fb_pack* pack, const fb_attn_shape* sh, int* pitch_out);
+hipError_t launch_window_prologue(const void* q_in, void* q_out, const void* k_new,
+                                  const void* v_new, void* k_cache, void* v_cache,
+                                  const int32_t* page_table, const fb_pack* pack,
+                                  const fb_attn_shape* sh, double rope_base,
+                                  hipStream_t stream);
+
 struct LmSizes {
     int n_rtiles;        // 256-token tiles over row_cap
     int n_vtiles;        // 256-id vocabulary tiles

@@ -293,3 +293,65 @@ def test_lmhead_accumulation_bound_covers_float32_products():
         f32 = (f32 + np.outer(H[:, i], Wt[:, i]).astype(np.float32)).astype(np.float32)
     bound = lmhead.accumulation_bound(H, Wt)
     assert np.all(np.abs(f32 - exact).max(axis=1) <= bound)
+
+
+# ---- RoPE and the window prologue ------------------------------------------
+def test_rope_position_zero_is_identity_and_norms_are_kept():
+    from oracle import rope
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((5, 3, 16))
+    assert np.allclose(rope.rope(x, np.zeros(5), 10000.0), x, atol=1e-15)
+    y = rope.rope(x, rng.integers(0, 50000, size=5), 10000.0)
+    # each (j, j + d/2) pair keeps its length
+    pn = lambda z: z[..., :8] ** 2 + z[..., 8:] ** 2
+    assert np.allclose(pn(y), pn(x), rtol=1e-12)
+
+
+def test_rope_scores_depend_on_relative_position_only():
+    """<rope(q, m), rope(k, n)> is a function of m - n: the property RoPE is
+    built for (RoFormer, Sec. 3.4)."""
+    from oracle import rope
+    rng = np.random.default_rng(9)
+    q = rng.standard_normal((1, 1, 32))
+    k = rng.standard_normal((1, 1, 32))
+    dot = lambda m, n: float(np.sum(rope.rope(q, [m], 500.0) * rope.rope(k, [n], 500.0)))
+    assert abs(dot(7, 3) - dot(1007, 1003)) < 1e-10
+    assert abs(dot(3, 7) - dot(40, 44)) < 1e-10
+    assert abs(dot(7, 3) - dot(3, 7)) > 1e-6          # but not symmetric in general
+
+
+def test_rope_matches_the_complex_rotation():
+    """Pair j as the complex number x_j + i x_{j+d/2} is multiplied by
+    e^(i p theta_j), theta_j = base^(-2j/d)."""
+    from oracle import rope
+    rng = np.random.default_rng(10)
+    x = rng.standard_normal((1, 1, 8))
+    p, base = 123, 10000.0
+    y = rope.rope(x, [p], base)[0, 0]
+    for j in range(4):
+        z = complex(x[0, 0, j], x[0, 0, j + 4]) * np.exp(1j * p * base ** (-2 * j / 8))
+        assert abs(y[j] - z.real) < 1e-12 and abs(y[j + 4] - z.imag) < 1e-12
+
+
+def test_window_prologue_rotates_live_rows_and_writes_only_the_window():
+    from oracle import rope
+    from oracle import pack as opack
+    st = _state([4, 9], 3, [0, 1], [2, 3])
+    packed = opack.pack_wavefronts(st, 2, 4, opack.PADDED)
+    rng = np.random.default_rng(11)
+    cap = packed["cap"]
+    q = rng.standard_normal((cap, 2, 8))
+    kn = rng.standard_normal((cap, 1, 8))
+    vn = rng.standard_normal((cap, 1, 8))
+    K = [rng.standard_normal((30, 1, 8)) for _ in range(2)]
+    V = [rng.standard_normal((30, 1, 8)) for _ in range(2)]
+    q2, K2, V2 = rope.window_prologue(q, kn, vn, K, V, packed, 10000.0)
+    dead = packed["row_req"] < 0
+    assert np.array_equal(q2[dead], q[dead])
+    for r in np.flatnonzero(~dead):
+        b, p = packed["row_req"][r], packed["row_pos"][r]
+        assert np.allclose(q2[r], rope.rope(q[r][None], [p], 10000.0)[0], atol=1e-15)
+        assert np.allclose(K2[b][p], rope.rope(kn[r][None], [p], 10000.0)[0], atol=1e-15)
+        assert np.array_equal(V2[b][p], vn[r])
+    o0 = 4 + 0 * 4
+    assert np.array_equal(K2[0][:o0], K[0][:o0])          # frozen prefix untouched

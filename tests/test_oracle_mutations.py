@@ -55,6 +55,10 @@ MUTATIONS = [
      "LM head takes the wrong operand orientation"),
     ("lmhead.py", "gamma = D * u / (1.0 - D * u)", "gamma = u",
      "accumulation bound without the length factor"),
+    ("rope.py", "[lo * c - hi * s, hi * c + lo * s]", "[lo * c + hi * s, hi * c - lo * s]",
+     "RoPE rotates the wrong way"),
+    ("rope.py", "inv = base ** (-2.0 * j / d)", "inv = base ** (-1.0 * j / d)",
+     "RoPE frequency exponent"),
 ]
 
 
