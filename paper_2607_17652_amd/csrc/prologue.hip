@@ -3,9 +3,11 @@
 // fused with the Eq. 6 window KV write, so the fresh keys are rotated and
 // land in the paged cache in one pass.
 //
-// rope_kv_kernel  one workgroup per live block (bl rows of one request):
+// rope_kv_kernel  one workgroup per (live block of bl rows, KV head c): the
+//                 g = Hq/Hkv query heads of c, key head c and value head c;
 //                 the block's cos/sin table (positions x d/2 pairs, angles
-//                 in float64, values rounded to float) in LDS; queries
+//                 formed and reduced to [-pi, pi] in float64, sin/cos in
+//                 float) in LDS; queries
 //                 rotated in place or into q_out; keys rotated and written to
 //                 their absolute slots of the K cache; values staged in LDS
 //                 and written key-innermost to the V cache.  Pair j of a head
@@ -17,6 +19,8 @@ namespace fb {
 namespace {
 
 constexpr int kRopeThreads = 256;
+constexpr double k2Pi = 6.283185307179586;
+constexpr double kInv2Pi = 0.15915494309189535;
 
 struct ThetaTable {
     double t[64];   // base^(-2j/d), j < d/2 <= 64
@@ -81,7 +85,9 @@ rope_kv_kernel(const T* __restrict__ q_in, T* __restrict__ q_out, const T* __res
     float2* tab = reinterpret_cast<float2*>(rope_smem);   // [bl][D/2] (cos, sin)
     T* vs = reinterpret_cast<T*>(rope_smem);              // later: [bl][pitch]
     const int t = blockIdx.x;
+    const int c = blockIdx.y;
     if (t >= pv.hdr[kHdrTiles]) return;
+    const int g = Hq / Hkv;
     const int32_t* tile = pv.tiles + (size_t)t * kTileInts;
     const int b = tile[kTB];
     const int row0 = tile[kTRow0];
@@ -93,53 +99,54 @@ rope_kv_kernel(const T* __restrict__ q_in, T* __restrict__ q_out, const T* __res
     for (int e = threadIdx.x; e < bl * half; e += kRopeThreads) {
         const int i = e / half;
         const int j = e % half;
+        // angle in float64, reduced to [-pi, pi] in float64, then float sin/cos
         const double a = (double)(pos0 + i) * theta.t[j];
-        double s, c;
-        sincos(a, &s, &c);
-        tab[e] = make_float2((float)c, (float)s);
+        const double r = a - rint(a * kInv2Pi) * k2Pi;
+        float s, c;
+        sincosf((float)r, &s, &c);
+        tab[e] = make_float2(c, s);
     }
     __syncthreads();
 
-    // queries
-    for (int e = threadIdx.x; e < bl * Hq * ng; e += kRopeThreads) {
-        const int g = e % ng;
-        const int hh = (e / ng) % Hq;
-        const int i = e / (ng * Hq);
-        const size_t base = ((size_t)(row0 + i) * Hq + hh) * D + g * 8;
+    // queries of the heads that read KV head c
+    for (int e = threadIdx.x; e < bl * g * ng; e += kRopeThreads) {
+        const int gi = e % ng;
+        const int hh = c * g + (e / ng) % g;
+        const int i = e / (ng * g);
+        const size_t base = ((size_t)(row0 + i) * Hq + hh) * D + gi * 8;
         float lo[8], hi[8];
         Vec8<T>::load(q_in + base, lo);
         Vec8<T>::load(q_in + base + half, hi);
-        rotate8(lo, hi, tab + i * half + g * 8);
+        rotate8(lo, hi, tab + i * half + gi * 8);
         Vec8<T>::store(q_out + base, lo);
         Vec8<T>::store(q_out + base + half, hi);
     }
     // keys: rotated straight into their absolute slots
-    for (int e = threadIdx.x; e < bl * Hkv * ng; e += kRopeThreads) {
-        const int g = e % ng;
-        const int c = (e / ng) % Hkv;
-        const int i = e / (ng * Hkv);
+    for (int e = threadIdx.x; e < bl * ng; e += kRopeThreads) {
+        const int gi = e % ng;
+        const int i = e / ng;
         const int pos = pos0 + i;
         const int pidx = pos / ps;
         const int page = pidx < max_pages ? pt[pidx] : -1;
         if (page < 0 || page >= num_pages) {
-            if (g == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
+            if (gi == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
             continue;
         }
-        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + g * 8;
+        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + gi * 8;
         float lo[8], hi[8];
         Vec8<T>::load(k_new + src, lo);
         Vec8<T>::load(k_new + src + half, hi);
-        rotate8(lo, hi, tab + i * half + g * 8);
-        T* dst = k_cache + (((size_t)page * Hkv + c) * ps + (pos % ps)) * D + g * 8;
+        rotate8(lo, hi, tab + i * half + gi * 8);
+        T* dst = k_cache + (((size_t)page * Hkv + c) * ps + (pos % ps)) * D + gi * 8;
         Vec8<T>::store(dst, lo);
         Vec8<T>::store(dst + half, hi);
     }
     __syncthreads();   // the table's LDS is reused for the values below
 
-    // values: key-innermost rows of the V cache, head by head
+    // values of head c: key-innermost rows of the V cache
     constexpr int VEC = 16 / sizeof(T);
     const int dch = D / VEC;
-    for (int c = 0; c < Hkv; ++c) {
+    {
         for (int e = threadIdx.x; e < bl * dch; e += kRopeThreads) {
             const int i = e / dch;
             const int dc = e % dch;
@@ -205,7 +212,7 @@ hipError_t launch_window_prologue(const void* q_in, void* q_out, const void* k_n
     for (int j = 0; j < D / 2; ++j) th.t[j] = pow(rope_base, -2.0 * j / D);
     int pitch = 0;
     const size_t smem = prologue_smem_bytes(pack, sh, &pitch);
-    const dim3 grid(pack->tile_cap);
+    const dim3 grid(pack->tile_cap, sh->Hkv);
     if (sh->dtype == FB_BF16)
         hipLaunchKernelGGL(rope_kv_kernel<uint16_t>, grid, dim3(kRopeThreads), smem, stream,
                            static_cast<const uint16_t*>(q_in), static_cast<uint16_t*>(q_out),
