@@ -367,9 +367,9 @@ def loop_bench(torch, fb, synth, DecodeLoop):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not "
-              f"supported (requests are independent, see the sharding notes)",
-              file=sys.stderr)
+        print(f"bench.py: the library runs one GPU per process; --gpus {args.gpus} is not "
+              f"supported here (requests are independent: each GPU would run this step on "
+              f"its own share of them)", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:
         copy_probe()
