@@ -68,6 +68,8 @@ def test_serve256_sampled_requests():
     dict(bl=64, page_size=64, W_max=4, window=("uniform", 1, 4)),   # Table 2 lengths
     dict(bl=96, page_size=32, W_max=3, window=("fixed", 3)),        # bl not a power of 2
     dict(bl=128, page_size=128, W_max=5, window=("fixed", 5), prefix_jitter=40),
+    dict(bl=1, page_size=8, W_max=3, window=("fixed", 3), prefix_jitter=3),   # one-token blocks
+    dict(bl=8, page_size=8, W_max=6, window=("uniform", 1, 6)),             # pages of 8, W = 6
     dict(V=1001, prefix_jitter=5),                  # unaligned logit rows
     dict(B=5, layout="padded", window=("uniform", 1, 3)),
 ])
