@@ -44,6 +44,8 @@ def parse_args():
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the HIP-graph replay of the K steps")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the steps timed after a cache flush")
     ap.add_argument("--no-loop", action="store_true",
                     help="skip the whole-decode loop runs on the synthetic model")
     ap.add_argument("--no-lmhead", action="store_true",
@@ -193,6 +195,27 @@ def cpu_baseline(wl, host, t, budget_s, seed):
                       f"pack, KV write, attention, vocab reduction, update in fp64 "
                       f"numpy; {spent:.1f} s; matmuls on {blas_threads} BLAS "
                       f"threads, the rest on one"}
+
+
+def cold_steps(torch, one_step, step, K, nph, flush_bytes=1 << 30):
+    """Each of K steps timed alone (HIP events on the launch stream) right
+    after 1 GiB has been written, which evicts the 256 MB last-level cache
+    and the L2s: the step's inputs come from HBM.  Every step starts from a
+    fresh copy of the pristine request state.  Median and mean."""
+    flush = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda")
+    pristine = (step.st, step.tokens, step.pe, step.fin)
+    times = []
+    for i in range(K):
+        state = tuple(x.clone() for x in pristine)
+        flush.fill_(i & 255)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)]
+        one_step(i, ev, state)
+        torch.cuda.synchronize()
+        times.append(ev[0].elapsed_time(ev[nph]))
+    del flush
+    import numpy as np
+    return {"ms_per_step_median": float(np.median(times)), "ms_per_step_mean": float(np.mean(times)),
+            "steps": K, "flush_bytes": flush_bytes}
 
 
 def graph_replay(torch, fb, step, one_step, copies, K, W):
@@ -436,7 +459,9 @@ def main():
     ph = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1])
                             for i in range(K)])) for j, n in enumerate(names)}
     ms_step = wall * 1e3 / K
+    step_ms = [events[i][0].elapsed_time(events[i][nph]) for i in range(K)]
     graph = None if args.no_graph else graph_replay(torch, fb, step, one_step, copies, K, W)
+    cold = None if args.no_cold else cold_steps(torch, one_step, step, K, nph)
     t_attn = ph["attention"] * 1e-3
     t_voc = ph["vocab_reduce"] * 1e-3
     t_upd = (ph["vocab_reduce"] + ph["update_apply"]) * 1e-3
@@ -464,6 +489,7 @@ def main():
         "value": n_live / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms_step,
+        "ms_per_step_median_events": float(np.median(step_ms)),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv,
@@ -478,6 +504,8 @@ def main():
     }
     if graph is not None:
         out["graph"] = graph
+    if cold is not None:
+        out["cold"] = cold
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
