@@ -33,6 +33,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kRowsPerWg = 128;     // 4 waves x 32 query rows
 constexpr int kAttnThreads = 256;
+constexpr int kWgsPerCu = 3;          // resident attention workgroups per CU
 constexpr int kKeyTile = 32;
 constexpr int kMinChunkTiles = 4;   // never split below 128 keys
 constexpr int kMaxSplits = 64;      // splits of one unit the combine can merge
@@ -306,7 +307,7 @@ __device__ inline void wait_vm(int n) {
 // FAST: pages hold whole key tiles (page_size >= 32), so a tile's loads share
 // one scalar base; otherwise each lane picks its page.
 template <int D, bool FAST>
-__global__ void __launch_bounds__(kAttnThreads, 3)
+__global__ void __launch_bounds__(kAttnThreads, kWgsPerCu)
 attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_cache,
                  const uint16_t* __restrict__ v_cache,
                  const int32_t* __restrict__ page_table, PackView pv, AttnWs ws,
@@ -973,7 +974,10 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
     z.rows_per_unit = pack->bl * g;
     z.row_groups = (z.rows_per_unit + kRowsPerWg - 1) / kRowsPerWg;
     z.unit_cap = pack->tile_cap * sh->Hkv * z.row_groups;
-    z.target_items = 8 * (cu_count > 0 ? cu_count : 256);
+    // One item per workgroup the chip holds at once (kWgsPerCu per CU): more
+    // splits cost more in partial writes, the merge and per-item start-up
+    // than they win in balance (measured: 8 per CU was 2-25% slower).
+    z.target_items = kWgsPerCu * (cu_count > 0 ? cu_count : 256);
     z.item_cap = z.unit_cap + z.target_items;
     z.slot_cap = 2 * z.target_items;
     const size_t D = sh->head_dim;
