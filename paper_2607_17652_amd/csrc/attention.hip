@@ -56,18 +56,69 @@ struct AttnWs {
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / 64;
 
-__device__ long long wg_sum_ll(long long v, long long* lds) {
+// Workgroup sum of v[0] and maximum of v[1] (one pair of barriers): each
+// wave reduces its 64 lanes, then every wave reduces the kPlanWaves wave
+// results itself and broadcasts lane 0's (no serial loop on one thread).
+__device__ void wg_sum_max(long long (&v)[2], long long (*lds)[kPlanWaves]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    if (lane == 0) lds[wave] = v;
+    for (int off = 32; off > 0; off >>= 1) {
+        v[0] += __shfl_xor(v[0], off, 64);
+        const long long o = __shfl_xor(v[1], off, 64);
+        if (o > v[1]) v[1] = o;
+    }
+    if (lane == 0) {
+        lds[0][wave] = v[0];
+        lds[1][wave] = v[1];
+    }
     __syncthreads();
-    long long s = 0;
-    for (int w = 0; w < kPlanWaves; ++w) s += lds[w];
+    long long sm = lane < kPlanWaves ? lds[0][lane] : 0;
+    long long mx = lane < kPlanWaves ? lds[1][lane] : 0;
+#pragma unroll
+    for (int off = kPlanWaves / 2; off > 0; off >>= 1) {
+        sm += __shfl_xor(sm, off, 64);
+        const long long o = __shfl_xor(mx, off, 64);
+        if (o > mx) mx = o;
+    }
+    v[0] = __shfl(sm, 0, 64);
+    v[1] = __shfl(mx, 0, 64);
     __syncthreads();
-    return s;
 }
 
+// Exclusive scans of two ints per thread across the workgroup (one pair of
+// barriers for both), and their totals.
+__device__ void wg_excl_scan2(int a, int b, int2* lds, int* ea, int* eb, int* ta, int* tb) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = a, y = b;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int xu = __shfl_up(x, off, 64), yu = __shfl_up(y, off, 64);
+        if (lane >= off) {
+            x += xu;
+            y += yu;
+        }
+    }
+    if (lane == 63) lds[wave] = make_int2(x, y);
+    __syncthreads();
+    int2 w = lane < kPlanWaves ? lds[lane] : make_int2(0, 0);
+#pragma unroll
+    for (int off = 1; off < kPlanWaves; off <<= 1) {
+        const int xu = __shfl_up(w.x, off, 64), yu = __shfl_up(w.y, off, 64);
+        if (lane >= off) {
+            w.x += xu;
+            w.y += yu;
+        }
+    }
+    const int bx = __shfl(w.x, wave > 0 ? wave - 1 : 0, 64);
+    const int by = __shfl(w.y, wave > 0 ? wave - 1 : 0, 64);
+    *ea = (wave > 0 ? bx : 0) + x - a;
+    *eb = (wave > 0 ? by : 0) + y - b;
+    *ta = __shfl(w.x, kPlanWaves - 1, 64);
+    *tb = __shfl(w.y, kPlanWaves - 1, 64);
+    __syncthreads();
+}
+
+// Exclusive scan of one int per thread across the workgroup, and the total.
 __device__ int wg_excl_scan(int v, int* lds, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int x = v;
@@ -78,28 +129,17 @@ __device__ int wg_excl_scan(int v, int* lds, int* total) {
     }
     if (lane == 63) lds[wave] = x;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int w = 0; w < kPlanWaves; ++w) {
-            int t = lds[w];
-            lds[w] = acc;
-            acc += t;
-        }
-        lds[kPlanWaves] = acc;
+    // every wave scans the wave totals itself
+    int w = lane < kPlanWaves ? lds[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < kPlanWaves; off <<= 1) {
+        int y = __shfl_up(w, off, 64);
+        if (lane >= off) w += y;
     }
+    const int before = wave > 0 ? __shfl(w, wave - 1, 64) : 0;
+    *total = __shfl(w, kPlanWaves - 1, 64);
     __syncthreads();
-    const int excl = lds[wave] + x - v;
-    *total = lds[kPlanWaves];
-    __syncthreads();
-    return excl;
-}
-
-// Key tiles of tile t (every unit of a tile has the same key range); 0 (skip)
-// when its keys run past the page table.
-__device__ inline int tile_key_tiles(const int32_t* tiles, int t, long long max_keys) {
-    const int kv = tiles[(size_t)t * kTileInts + kTKvLen];
-    if ((long long)kv > max_keys) return 0;
-    return (kv + kKeyTile - 1) / kKeyTile;
+    return before + x - v;
 }
 
 // Items are written longest first (a counting sort on their key-tile count,
@@ -108,73 +148,115 @@ __device__ inline int tile_key_tiles(const int32_t* tiles, int t, long long max_
 // plan works per tile: the per_tile units of a tile (kv-heads x row groups)
 // have the same key range, so they get the same split and adjacent items
 // (with 8 kv-heads the round-robin dispatch then keeps each kv-head on one
-// XCD).
+// XCD).  Thread i handles tiles i, i + kPlanThreads, ...; the fields of its
+// first kPlanCache tiles are read once and kept in registers.
 constexpr int kLenBuckets = kPlanThreads;
+constexpr int kPlanCache = 4;
+
+struct PlanTile {
+    int kt;   // key tiles of the tile; 0 (skipped, error) past the page table
+    int kr;   // sort key: key tiles of its request's last live block
+    int kv;   // keys the tile attends to
+};
+
+__device__ inline PlanTile plan_tile(const int32_t* tiles, int t, int n_tiles, long long max_keys) {
+    PlanTile p{0, 0, 0};
+    if (t >= n_tiles) return p;
+    const int32_t* tl = tiles + (size_t)t * kTileInts;
+    p.kv = tl[kTKvLen];
+    p.kt = (long long)p.kv > max_keys ? 0 : (p.kv + kKeyTile - 1) / kKeyTile;
+    // the blocks of one request read the same prefix K/V: keyed by the
+    // request's longest block they land in the same buckets next to each
+    // other and run together, sharing the prefix through L2
+    const long long blen = tl[kTKvLen] - tl[kTPos0];
+    const long long kv_last = tl[kTO] + (long long)tl[kTW] * blen;
+    const long long kr = (kv_last + kKeyTile - 1) / kKeyTile;
+    p.kr = kr > p.kt ? (int)kr : p.kt;
+    return p;
+}
 
 __global__ void __launch_bounds__(kPlanThreads)
 plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             int target_items, int fixed_chunk_tiles, long long max_keys) {
-    __shared__ long long sum_lds[kPlanWaves];
+    __shared__ long long sum_lds[2][kPlanWaves];
     __shared__ int scan_lds[kPlanWaves + 1];
+    __shared__ int2 pair_lds[kPlanWaves];
     __shared__ int bucket[kLenBuckets];
     const int n_tiles = pv.hdr[kHdrTiles];
     const int per_tile = Hkv * RG;
     const int n_units = n_tiles * per_tile;
+    const int n_rounds = (n_tiles + kPlanThreads - 1) / kPlanThreads;
 
-    long long my_tiles = 0;
-    for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads)
-        my_tiles += tile_key_tiles(pv.tiles, t, max_keys);
-    const long long total_tiles = wg_sum_ll(my_tiles, sum_lds) * per_tile;
+    PlanTile cache[kPlanCache];
+#pragma unroll
+    for (int j = 0; j < kPlanCache; ++j)
+        cache[j] = plan_tile(pv.tiles, j * kPlanThreads + threadIdx.x, n_tiles, max_keys);
+    // this thread's tile of round c (zeros past the end)
+    auto tile_of = [&](int c) -> PlanTile {
+        if (c >= kPlanCache)
+            return plan_tile(pv.tiles, c * kPlanThreads + threadIdx.x, n_tiles, max_keys);
+        PlanTile p = cache[0];
+#pragma unroll
+        for (int j = 1; j < kPlanCache; ++j)
+            if (c == j) p = cache[j];
+        return p;
+    };
 
-    long long chunk = fixed_chunk_tiles;
-    if (chunk <= 0) {
-        chunk = (total_tiles + target_items - 1) / target_items;
-        if (chunk < kMinChunkTiles) chunk = kMinChunkTiles;
+    // key tiles summed over the tiles, and the longest tile
+    long long red[2] = {0, 0};
+    for (int c = 0; c < n_rounds; ++c) {
+        const int kt = tile_of(c).kt;
+        red[0] += kt;
+        if (kt > red[1]) red[1] = kt;
     }
-    // Grow the split size until the items and partial slots fit and no unit
-    // has more splits than the combine merges.
-    for (;;) {
-        long long my_items = 0, my_slots = 0, my_over = 0;
-        for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads) {
-            const long long kt = tile_key_tiles(pv.tiles, t, max_keys);
-            const long long ns = (kt + chunk - 1) / chunk;
-            my_items += ns * per_tile;
-            if (ns > 1) my_slots += ns * per_tile;
-            if (ns > kMaxSplits) my_over += 1;
+    wg_sum_max(red, sum_lds);
+    const long long total_tiles = red[0] * per_tile;
+    const long long kt_max = red[1];
+
+    // Split size.  With chunk >= total_tiles / target_items the items and
+    // the partial slots always fit: a unit of kt key tiles makes
+    // ceil(kt/chunk) <= kt/chunk + 1 items, so all units make at most
+    // total_tiles/chunk + n_units <= item_cap, and a split unit's
+    // ceil(kt/chunk) < 2 kt/chunk slots sum to at most 2 target_items =
+    // slot_cap.  A chunk >= kt_max / kMaxSplits keeps every unit within the
+    // splits the combine merges.  A requested split size is doubled until
+    // both hold.  (Sizes stay below 2^30 key tiles: 32-bit math below.)
+    long long need = (total_tiles + target_items - 1) / target_items;
+    const long long need_m = (kt_max + kMaxSplits - 1) / kMaxSplits;
+    if (need_m > need) need = need_m;
+    long long chunk_ll;
+    if (fixed_chunk_tiles > 0) {
+        chunk_ll = fixed_chunk_tiles;
+        while (chunk_ll < need) chunk_ll *= 2;
+    } else {
+        chunk_ll = need > kMinChunkTiles ? need : kMinChunkTiles;
+    }
+    if (chunk_ll >= (1 << 30)) {
+        // beyond any real cache (over 2^30 key tiles per item): nothing is
+        // planned and the first tile's request is flagged
+        if (threadIdx.x == 0) {
+            record_error(pv.hdr, pv.tiles[kTB], FB_DERR_PAGE);
+            ws.counts[kCItems] = 0;
+            ws.counts[kCUnits] = 0;
+            ws.counts[kCChunk] = -1;
         }
-        const long long items = wg_sum_ll(my_items, sum_lds);
-        const long long slots = wg_sum_ll(my_slots, sum_lds);
-        const long long over = wg_sum_ll(my_over, sum_lds);
-        if (items <= item_cap && slots <= slot_cap && over == 0) break;
-        chunk *= 2;
+        return;
     }
+    const int chunk = (int)chunk_ll;
 
     // Histogram of item lengths, then each bucket's first position with the
     // longest bucket first.
-    auto len_key = [&](long long kt, int k) -> int {
-        long long len = kt - (long long)k * chunk;
+    auto len_key = [&](int kt, int k) -> int {
+        int len = kt - k * chunk;
         if (len > chunk) len = chunk;
-        return len >= kLenBuckets - 1 ? kLenBuckets - 1 : (int)len;
-    };
-    // Sort key of a tile's items: the key tiles of its request's longest
-    // (last) live block, so the blocks of one request, which read the same
-    // prefix K/V, land in the same buckets next to each other and run
-    // together (sharing the prefix through L2) even when many requests have
-    // equal lengths.
-    auto sort_tiles = [&](int t, long long kt) -> long long {
-        const int32_t* tl = pv.tiles + (size_t)t * kTileInts;
-        const long long blen = tl[kTKvLen] - tl[kTPos0];
-        const long long kv_last = tl[kTO] + (long long)tl[kTW] * blen;
-        const long long kr = (kv_last + kKeyTile - 1) / kKeyTile;
-        return kr > kt ? kr : kt;
+        return len >= kLenBuckets - 1 ? kLenBuckets - 1 : len;
     };
     bucket[threadIdx.x] = 0;
     __syncthreads();
-    for (int t = threadIdx.x; t < n_tiles; t += kPlanThreads) {
-        const long long kt = tile_key_tiles(pv.tiles, t, max_keys);
-        const int ns = (int)((kt + chunk - 1) / chunk);
-        const long long kr = sort_tiles(t, kt);
-        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(kr, k)], per_tile);
+    for (int c = 0; c < n_rounds; ++c) {
+        const PlanTile p = tile_of(c);
+        const int ns = (p.kt + chunk - 1) / chunk;
+        for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
     }
     __syncthreads();
     {
@@ -187,18 +269,17 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     }
 
     int items_before = 0, slots_before = 0;
-    for (int base = 0; base < n_tiles; base += kPlanThreads) {
-        const int t = base + threadIdx.x;
-        int ns = 0, kt = 0, kv = 0;
-        if (t < n_tiles) {
-            kt = tile_key_tiles(pv.tiles, t, max_keys);
-            kv = pv.tiles[(size_t)t * kTileInts + kTKvLen];
-            ns = (int)((kt + chunk - 1) / chunk);
-            if (kt == 0) record_error(pv.hdr, pv.tiles[(size_t)t * kTileInts + kTB], FB_DERR_PAGE);
-        }
-        int tot_items, tot_slots;
-        (void)wg_excl_scan(ns * per_tile, scan_lds, &tot_items);
-        const int slot_t = slots_before + wg_excl_scan(ns > 1 ? ns * per_tile : 0, scan_lds, &tot_slots);
+    for (int c = 0; c < n_rounds; ++c) {
+        const int t = c * kPlanThreads + threadIdx.x;
+        const PlanTile p = tile_of(c);
+        const int ns = (p.kt + chunk - 1) / chunk;
+        if (t < n_tiles && p.kt == 0)
+            record_error(pv.hdr, pv.tiles[(size_t)t * kTileInts + kTB], FB_DERR_PAGE);
+        int tot_items, tot_slots, ex_items, ex_slots;
+        wg_excl_scan2(ns * per_tile, ns > 1 ? ns * per_tile : 0, pair_lds, &ex_items, &ex_slots,
+                      &tot_items, &tot_slots);
+        (void)ex_items;
+        const int slot_t = slots_before + ex_slots;
         if (t < n_tiles) {
             // unit j of the tile owns slots slot_t + j*ns .. + ns-1
             for (int j = 0; j < per_tile; ++j) {
@@ -206,13 +287,13 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
                 ws.units[(size_t)u * 2 + kUSplits] = ns;
                 ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot_t + j * ns : -1;
             }
-            const long long kr = sort_tiles(t, kt);
             for (int k = 0; k < ns; ++k) {
-                const int pos = atomicAdd(&bucket[len_key(kr, k)], per_tile);
+                const int pos = atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
                 const long long kb = (long long)k * chunk * kKeyTile;
-                long long ke = kb + chunk * kKeyTile;
-                if (ke > kv) ke = kv;
+                long long ke = kb + (long long)chunk * kKeyTile;
+                if (ke > p.kv) ke = p.kv;
                 for (int j = 0; j < per_tile; ++j) {
+                    if (pos + j >= item_cap) break;   // cannot happen: the loop above fits the caps
                     int32_t* it = ws.items + (size_t)(pos + j) * 4;
                     it[kIUnit] = t * per_tile + j;
                     it[kIKb] = (int)kb;
@@ -225,9 +306,9 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         slots_before += tot_slots;
     }
     if (threadIdx.x == 0) {
-        ws.counts[kCItems] = items_before;
+        ws.counts[kCItems] = items_before < item_cap ? items_before : item_cap;
         ws.counts[kCUnits] = n_units;
-        ws.counts[kCChunk] = (int)(chunk * kKeyTile);
+        ws.counts[kCChunk] = chunk < (1 << 30) / kKeyTile ? chunk * kKeyTile : -1;   // keys
     }
 }
 

@@ -16,7 +16,8 @@ constexpr int kPackThreads = 1024;
 constexpr int kPackWaves = kPackThreads / 64;
 
 // Exclusive scan of one int per thread across the workgroup; also returns the
-// total.  `lds` holds kPackWaves + 1 ints.
+// total.  Each wave scans its 64 values, then every wave scans the
+// kPackWaves wave totals itself.  `lds` holds kPackWaves ints.
 __device__ int workgroup_exclusive_scan(int v, int* lds, int* total) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -28,20 +29,16 @@ __device__ int workgroup_exclusive_scan(int v, int* lds, int* total) {
     }
     if (lane == 63) lds[wave] = x;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int w = 0; w < kPackWaves; ++w) {
-            int t = lds[w];
-            lds[w] = acc;
-            acc += t;
-        }
-        lds[kPackWaves] = acc;
+    int w = lane < kPackWaves ? lds[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < kPackWaves; off <<= 1) {
+        int y = __shfl_up(w, off, 64);
+        if (lane >= off) w += y;
     }
+    const int before = __shfl(w, wave > 0 ? wave - 1 : 0, 64);
+    *total = __shfl(w, kPackWaves - 1, 64);
     __syncthreads();
-    int excl = lds[wave] + x - v;
-    *total = lds[kPackWaves];
-    __syncthreads();
-    return excl;
+    return (wave > 0 ? before : 0) + x - v;
 }
 
 __global__ void __launch_bounds__(kPackThreads)
