@@ -140,8 +140,11 @@ typedef struct fb_attn_shape {
     int32_t page_size;     /* power of two; FB_BF16 needs >= 8                 */
     int32_t max_pages;     /* columns of page_table                            */
     int32_t num_pages;     /* physical pages in each cache                     */
-    int32_t kv_split;      /* keys per split-KV partition, a multiple of 32;
-                              0 chooses one from the device's CU count         */
+    int32_t kv_split;      /* keys per split-KV partition, a multiple of 32
+                              (doubled on the device while the partitions
+                              would overflow the workspace's item or partial
+                              slots or exceed 64 per unit); 0 chooses one
+                              from the device's CU count                       */
     float   sm_scale;      /* <= 0 means 1/sqrt(head_dim)                      */
     int32_t reserved[3];
 } fb_attn_shape;
