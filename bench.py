@@ -218,6 +218,35 @@ def cold_steps(torch, one_step, step, K, nph, flush_bytes=1 << 30):
             "steps": K, "flush_bytes": flush_bytes}
 
 
+def hbm_probe(torch, nbytes=2 << 30, reps=5):
+    """Measured device-memory rates to set the vocabulary pass against (besides
+    the 8 TB/s vendor figure): a plain device copy (bytes read + written per
+    second) and torch's sum over a bf16 tensor (bytes read per second), each
+    the best of `reps` launches timed with events."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    xs = src.view(torch.bfloat16)
+
+    def best(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return min(ts)
+
+    t_copy = best(lambda: dst.copy_(src))
+    t_sum = best(lambda: xs.sum(dtype=torch.float32))
+    del src, dst, xs
+    return {"copy_GBps": 2 * nbytes / t_copy / 1e9, "sum_read_GBps": nbytes / t_sum / 1e9,
+            "bytes": nbytes, "note": "best of 5; copy counts bytes read + written"}
+
+
 def graph_replay(torch, fb, step, one_step, copies, K, W):
     """The same K steps captured once in a HIP graph and replayed.
 
@@ -506,6 +535,7 @@ def main():
         out["graph"] = graph
     if cold is not None:
         out["cold"] = cold
+    out["hbm_probe"] = hbm_probe(torch)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
