@@ -52,6 +52,13 @@ def test_long8_sampled_requests():
     run_and_compare("long8", reqs=[0, 5])
 
 
+def test_longest_prefix_hits_the_split_cap():
+    """One request with a 64K-key prefix and two live blocks: the split size
+    is raised until no unit has more than 64 pieces (the most the merge of
+    partial results takes), here 62-63 pieces of 33 key tiles per unit."""
+    run_and_compare("single", prefix=("fixed", 65536), window=("fixed", 2), W_max=2)
+
+
 def test_serve256_sampled_requests():
     rng = np.random.default_rng(7)
     reqs = sorted(rng.choice(256, size=12, replace=False).tolist())
