@@ -143,7 +143,8 @@ typedef struct fb_attn_shape {
     int32_t kv_split;      /* keys per split-KV partition, a multiple of 32
                               (doubled on the device while the partitions
                               would overflow the workspace's item or partial
-                              slots or exceed 64 per unit); 0 chooses one
+                              slots or exceed 64 per unit; a unit of at most
+                              1.5 partitions stays whole); 0 chooses one
                               from the device's CU count                       */
     float   sm_scale;      /* <= 0 means 1/sqrt(head_dim)                      */
     int32_t reserved[3];

@@ -246,16 +246,25 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
 
     // Histogram of item lengths, then each bucket's first position with the
     // longest bucket first.
+    // A unit of at most 1.5 chunks stays whole (a piece of half a chunk or
+    // less costs more in its partial result and merge than it saves in
+    // balance: measured 5% on hetero64's attention); longer units are cut
+    // into chunk-sized pieces and a shorter last one.  Either way a unit
+    // makes at most ceil(kt / chunk) items, so the bounds above hold.
+    auto nsplit = [&](int kt) -> int {
+        return 2LL * kt > 3LL * chunk ? (kt + chunk - 1) / chunk : (kt > 0 ? 1 : 0);
+    };
     auto len_key = [&](int kt, int k) -> int {
-        int len = kt - k * chunk;
-        if (len > chunk) len = chunk;
+        const int nsk = nsplit(kt);
+        int len = nsk == 1 ? kt : kt - k * chunk;
+        if (nsk > 1 && len > chunk) len = chunk;
         return len >= kLenBuckets - 1 ? kLenBuckets - 1 : len;
     };
     bucket[threadIdx.x] = 0;
     __syncthreads();
     for (int c = 0; c < n_rounds; ++c) {
         const PlanTile p = tile_of(c);
-        const int ns = (p.kt + chunk - 1) / chunk;
+        const int ns = nsplit(p.kt);
         for (int k = 0; k < ns; ++k) atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
     }
     __syncthreads();
@@ -272,7 +281,7 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     for (int c = 0; c < n_rounds; ++c) {
         const int t = c * kPlanThreads + threadIdx.x;
         const PlanTile p = tile_of(c);
-        const int ns = (p.kt + chunk - 1) / chunk;
+        const int ns = nsplit(p.kt);
         if (t < n_tiles && p.kt == 0)
             record_error(pv.hdr, pv.tiles[(size_t)t * kTileInts + kTB], FB_DERR_PAGE);
         int tot_items, tot_slots, ex_items, ex_slots;
@@ -290,7 +299,7 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             for (int k = 0; k < ns; ++k) {
                 const int pos = atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
                 const long long kb = (long long)k * chunk * kKeyTile;
-                long long ke = kb + (long long)chunk * kKeyTile;
+                long long ke = k == ns - 1 ? (long long)p.kv : kb + (long long)chunk * kKeyTile;
                 if (ke > p.kv) ke = p.kv;
                 for (int j = 0; j < per_tile; ++j) {
                     if (pos + j >= item_cap) break;   // cannot happen: the loop above fits the caps
