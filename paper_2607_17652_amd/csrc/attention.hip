@@ -42,12 +42,13 @@ constexpr float kRescaleSlack = 8.0f;  // lazy rescale: running max may lag by 2
 
 enum ItemField { kIUnit = 0, kIKb, kIKe, kISlot };
 enum UnitField { kUSplits = 0, kUSlot0 };
-enum CountField { kCItems = 0, kCUnits, kCChunk };
+enum CountField { kCItems = 0, kCUnits, kCChunk, kCSplit };
 
 struct AttnWs {
     int32_t* items;    // [item_cap][4]
     int32_t* units;    // [unit_cap][2]
     int32_t* counts;   // [4]
+    int32_t* split;    // [split_cap]: the units with more than one piece
     float* part_o;     // [slot_cap][128][D]
     float* part_lse;   // [slot_cap][128]
 };
@@ -85,36 +86,38 @@ __device__ void wg_sum_max(long long (&v)[2], long long (*lds)[kPlanWaves]) {
     __syncthreads();
 }
 
-// Exclusive scans of two ints per thread across the workgroup (one pair of
-// barriers for both), and their totals.
-__device__ void wg_excl_scan2(int a, int b, int2* lds, int* ea, int* eb, int* ta, int* tb) {
+// Exclusive scans of three ints per thread across the workgroup (one pair of
+// barriers for all three): v[i] becomes its exclusive prefix, tot[i] the
+// workgroup total.
+__device__ void wg_excl_scan3(int (&v)[3], int (&tot)[3], int3* lds) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int x = a, y = b;
+    int x[3] = {v[0], v[1], v[2]};
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        const int xu = __shfl_up(x, off, 64), yu = __shfl_up(y, off, 64);
-        if (lane >= off) {
-            x += xu;
-            y += yu;
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            const int u = __shfl_up(x[i], off, 64);
+            if (lane >= off) x[i] += u;
         }
     }
-    if (lane == 63) lds[wave] = make_int2(x, y);
+    if (lane == 63) lds[wave] = make_int3(x[0], x[1], x[2]);
     __syncthreads();
-    int2 w = lane < kPlanWaves ? lds[lane] : make_int2(0, 0);
+    const int3 l = lane < kPlanWaves ? lds[lane] : make_int3(0, 0, 0);
+    int w[3] = {l.x, l.y, l.z};
 #pragma unroll
     for (int off = 1; off < kPlanWaves; off <<= 1) {
-        const int xu = __shfl_up(w.x, off, 64), yu = __shfl_up(w.y, off, 64);
-        if (lane >= off) {
-            w.x += xu;
-            w.y += yu;
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+            const int u = __shfl_up(w[i], off, 64);
+            if (lane >= off) w[i] += u;
         }
     }
-    const int bx = __shfl(w.x, wave > 0 ? wave - 1 : 0, 64);
-    const int by = __shfl(w.y, wave > 0 ? wave - 1 : 0, 64);
-    *ea = (wave > 0 ? bx : 0) + x - a;
-    *eb = (wave > 0 ? by : 0) + y - b;
-    *ta = __shfl(w.x, kPlanWaves - 1, 64);
-    *tb = __shfl(w.y, kPlanWaves - 1, 64);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        const int before = __shfl(w[i], wave > 0 ? wave - 1 : 0, 64);
+        tot[i] = __shfl(w[i], kPlanWaves - 1, 64);
+        v[i] = (wave > 0 ? before : 0) + x[i] - v[i];
+    }
     __syncthreads();
 }
 
@@ -177,10 +180,10 @@ __device__ inline PlanTile plan_tile(const int32_t* tiles, int t, int n_tiles, l
 
 __global__ void __launch_bounds__(kPlanThreads)
 plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
-            int target_items, int fixed_chunk_tiles, long long max_keys) {
+            int split_cap, int target_items, int fixed_chunk_tiles, long long max_keys) {
     __shared__ long long sum_lds[2][kPlanWaves];
     __shared__ int scan_lds[kPlanWaves + 1];
-    __shared__ int2 pair_lds[kPlanWaves];
+    __shared__ int3 trio_lds[kPlanWaves];
     __shared__ int bucket[kLenBuckets];
     const int n_tiles = pv.hdr[kHdrTiles];
     const int per_tile = Hkv * RG;
@@ -239,6 +242,7 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             ws.counts[kCItems] = 0;
             ws.counts[kCUnits] = 0;
             ws.counts[kCChunk] = -1;
+            ws.counts[kCSplit] = 0;
         }
         return;
     }
@@ -277,24 +281,27 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         __syncthreads();
     }
 
-    int items_before = 0, slots_before = 0;
+    int items_before = 0, slots_before = 0, split_before = 0;
     for (int c = 0; c < n_rounds; ++c) {
         const int t = c * kPlanThreads + threadIdx.x;
         const PlanTile p = tile_of(c);
         const int ns = nsplit(p.kt);
         if (t < n_tiles && p.kt == 0)
             record_error(pv.hdr, pv.tiles[(size_t)t * kTileInts + kTB], FB_DERR_PAGE);
-        int tot_items, tot_slots, ex_items, ex_slots;
-        wg_excl_scan2(ns * per_tile, ns > 1 ? ns * per_tile : 0, pair_lds, &ex_items, &ex_slots,
-                      &tot_items, &tot_slots);
-        (void)ex_items;
-        const int slot_t = slots_before + ex_slots;
+        // items, partial slots and split units of this round's tiles
+        int ex[3] = {ns * per_tile, ns > 1 ? ns * per_tile : 0, ns > 1 ? per_tile : 0};
+        int tot[3];
+        wg_excl_scan3(ex, tot, trio_lds);
+        const int slot_t = slots_before + ex[1];
+        const int split_t = split_before + ex[2];
         if (t < n_tiles) {
-            // unit j of the tile owns slots slot_t + j*ns .. + ns-1
+            // unit j of the tile owns slots slot_t + j*ns .. + ns-1 and, when
+            // split, entry split_t + j of the list the merge walks
             for (int j = 0; j < per_tile; ++j) {
                 const int u = t * per_tile + j;
                 ws.units[(size_t)u * 2 + kUSplits] = ns;
                 ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot_t + j * ns : -1;
+                if (ns > 1 && split_t + j < split_cap) ws.split[split_t + j] = u;
             }
             for (int k = 0; k < ns; ++k) {
                 const int pos = atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
@@ -311,13 +318,15 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
                 }
             }
         }
-        items_before += tot_items;
-        slots_before += tot_slots;
+        items_before += tot[0];
+        slots_before += tot[1];
+        split_before += tot[2];
     }
     if (threadIdx.x == 0) {
         ws.counts[kCItems] = items_before < item_cap ? items_before : item_cap;
         ws.counts[kCUnits] = n_units;
         ws.counts[kCChunk] = chunk < (1 << 30) / kKeyTile ? chunk * kKeyTile : -1;   // keys
+        ws.counts[kCSplit] = split_before < split_cap ? split_before : split_cap;
     }
 }
 
@@ -889,7 +898,8 @@ template <>
 __device__ inline void store_out<float>(float* p, float v) { *p = v; }
 
 // Each split unit's rows are merged by kCombineParts workgroups of
-// kCombineRows rows: a row's per-split log-sum-exp weights go to LDS once,
+// kCombineRows rows (workgroup b takes entry b / kCombineParts of the plan's
+// list of split units, so the grid covers only units that can be split): a row's per-split log-sum-exp weights go to LDS once,
 // then every thread merges 16-byte columns of its rows, four splits' loads
 // in flight at a time.
 constexpr int kCombineRows = 32;
@@ -901,10 +911,11 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
                int g, int bl, int RG, int D) {
     __shared__ float wgt[kMaxSplits][kCombineRows];
     __shared__ float inv_den[kCombineRows];
-    const int u = blockIdx.x / kCombineParts;
+    const int su = blockIdx.x / kCombineParts;
     const int part = blockIdx.x % kCombineParts;
-    if (u >= ws.counts[kCUnits]) return;
-    const int ns = ws.units[(size_t)u * 2 + kUSplits];   // <= kMaxSplits (plan)
+    if (su >= ws.counts[kCSplit]) return;
+    const int u = ws.split[su];
+    const int ns = ws.units[(size_t)u * 2 + kUSplits];   // 2 .. kMaxSplits (plan)
     if (ns <= 1) return;
     const int slot0 = ws.units[(size_t)u * 2 + kUSlot0];
     const int rg = u % RG;
@@ -1070,6 +1081,7 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
     z.target_items = kWgsPerCu * (cu_count > 0 ? cu_count : 256);
     z.item_cap = z.unit_cap + z.target_items;
     z.slot_cap = 2 * z.target_items;
+    z.split_cap = z.target_items;   // a split unit holds at least two of the slots
     const size_t D = sh->head_dim;
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -1080,6 +1092,7 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
     z.off_items = take((size_t)z.item_cap * 4 * sizeof(int32_t));
     z.off_units = take((size_t)z.unit_cap * 2 * sizeof(int32_t));
     z.off_counts = take(4 * sizeof(int32_t));
+    z.off_split = take((size_t)z.split_cap * sizeof(int32_t));
     if (sh->dtype == FB_BF16) {
         z.off_part_o = take((size_t)z.slot_cap * kRowsPerWg * D * sizeof(float));
         z.off_part_lse = take((size_t)z.slot_cap * kRowsPerWg * sizeof(float));
@@ -1114,12 +1127,13 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     AttnWs ws{reinterpret_cast<int32_t*>(base + z.off_items),
               reinterpret_cast<int32_t*>(base + z.off_units),
               reinterpret_cast<int32_t*>(base + z.off_counts),
+              reinterpret_cast<int32_t*>(base + z.off_split),
               reinterpret_cast<float*>(base + z.off_part_o),
               reinterpret_cast<float*>(base + z.off_part_lse)};
     const int fixed_chunk = sh->kv_split > 0 ? sh->kv_split / kKeyTile : 0;
     const long long max_keys = (long long)sh->max_pages * sh->page_size;
     hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pv,
-                       ws, sh->Hkv, z.row_groups, z.item_cap, z.slot_cap,
+                       ws, sh->Hkv, z.row_groups, z.item_cap, z.slot_cap, z.split_cap,
                        z.target_items, fixed_chunk, max_keys);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1152,7 +1166,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.unit_cap * kCombineParts), dim3(kAttnThreads),
+    hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.split_cap * kCombineParts), dim3(kAttnThreads),
                        0, stream, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl,
                        z.row_groups, sh->head_dim);
     return hipGetLastError();

@@ -67,7 +67,8 @@ struct AttnPlanSizes {
     int item_cap;         // work items the plan may emit
     int slot_cap;         // split partial slots
     int target_items;     // automatic split target
-    size_t off_items, off_units, off_counts, off_part_o, off_part_lse, total;
+    int split_cap;        // units with more than one piece (slot_cap / 2)
+    size_t off_items, off_units, off_counts, off_split, off_part_o, off_part_lse, total;
 };
 AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
                               int cu_count);
