@@ -40,12 +40,15 @@ constexpr int kMaxSplits = 64;      // splits of one unit the combine can merge
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;  // lazy rescale: running max may lag by 2^8
 
-enum ItemField { kIUnit = 0, kIKb, kIKe, kISlot };
+// A work item: its unit, key range and partial slot, and the request and
+// first packed row of its tile (copied here so the attention workgroup's
+// first dependent loads are the item and then the page table).
+enum ItemField { kIUnit = 0, kIKb, kIKe, kISlot, kIB, kIRow0, kIItemInts = 8 };
 enum UnitField { kUSplits = 0, kUSlot0 };
 enum CountField { kCItems = 0, kCUnits, kCChunk, kCSplit };
 
 struct AttnWs {
-    int32_t* items;    // [item_cap][4]
+    int32_t* items;    // [item_cap][kIItemInts]
     int32_t* units;    // [unit_cap][2]
     int32_t* counts;   // [4]
     int32_t* split;    // [split_cap]: the units with more than one piece
@@ -160,13 +163,17 @@ struct PlanTile {
     int kt;   // key tiles of the tile; 0 (skipped, error) past the page table
     int kr;   // sort key: key tiles of its request's last live block
     int kv;   // keys the tile attends to
+    int b;    // request
+    int row0; // first packed row
 };
 
 __device__ inline PlanTile plan_tile(const int32_t* tiles, int t, int n_tiles, long long max_keys) {
-    PlanTile p{0, 0, 0};
+    PlanTile p{0, 0, 0, 0, 0};
     if (t >= n_tiles) return p;
     const int32_t* tl = tiles + (size_t)t * kTileInts;
     p.kv = tl[kTKvLen];
+    p.b = tl[kTB];
+    p.row0 = tl[kTRow0];
     p.kt = (long long)p.kv > max_keys ? 0 : (p.kv + kKeyTile - 1) / kKeyTile;
     // the blocks of one request read the same prefix K/V: keyed by the
     // request's longest block they land in the same buckets next to each
@@ -310,11 +317,10 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
                 if (ke > p.kv) ke = p.kv;
                 for (int j = 0; j < per_tile; ++j) {
                     if (pos + j >= item_cap) break;   // cannot happen: the loop above fits the caps
-                    int32_t* it = ws.items + (size_t)(pos + j) * 4;
-                    it[kIUnit] = t * per_tile + j;
-                    it[kIKb] = (int)kb;
-                    it[kIKe] = (int)ke;
-                    it[kISlot] = ns > 1 ? slot_t + j * ns + k : -1;
+                    int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(pos + j) * kIItemInts);
+                    it[0] = make_int4(t * per_tile + j, (int)kb, (int)ke,
+                                      ns > 1 ? slot_t + j * ns + k : -1);
+                    it[1] = make_int4(p.b, p.row0, 0, 0);
                 }
             }
         }
@@ -420,16 +426,19 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     constexpr int NCH = RG_::kPerThread;
     constexpr int CPR = D / 8;      // 16-byte chunks per K row
 
+    // The item's record is read together with the item count (the grid has
+    // item_cap workgroups, so the record is always inside the buffer).
     const int item = blockIdx.x;
-    if (item >= ws.counts[kCItems]) return;
-    const int32_t* it = ws.items + (size_t)item * 4;
+    const int32_t* it = ws.items + (size_t)item * kIItemInts;
     const int u = it[kIUnit], kb = it[kIKb], ke = it[kIKe], slot = it[kISlot];
+    const int b = it[kIB], row0 = it[kIRow0];
+    const int n_items = ws.counts[kCItems];
+    // (the empty asm keeps the compiler from sinking the record's loads below
+    // the count check, which would serialize the two round trips)
+    asm volatile("" :: "s"(u), "s"(kb), "s"(ke), "s"(slot), "s"(b), "s"(row0), "s"(n_items));
+    if (item >= n_items) return;
     const int rg = u % RG;
     const int c = (u / RG) % Hkv;
-    const int t = u / (RG * Hkv);
-    const int32_t* tile = pv.tiles + (size_t)t * kTileInts;
-    const int b = tile[kTB];
-    const int row0 = tile[kTRow0];
     const int32_t* pt = page_table + (size_t)b * max_pages;
 
     const int tid = threadIdx.x;
@@ -444,16 +453,16 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     const int hg = row_ok ? r % g : 0;
     const size_t q_off = ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D;
 
-    // Q fragments go to registers first; the empty asm makes the compiler
-    // finish these loads before any ring load is issued.
+    // Q fragments, loaded right after the first ring loads are issued so
+    // that both latencies overlap (the first wait covers both).
     bf16x8 qf[KK];
+    auto load_q = [&]() {
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-        if (row_ok) qf[kk] = *reinterpret_cast<const bf16x8*>(q + q_off + kk * 16 + h * 8);
-        else qf[kk] = bf16x8{};
-    }
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) asm volatile("" :: "v"(qf[kk]));
+        for (int kk = 0; kk < KK; ++kk) {
+            if (row_ok) qf[kk] = *reinterpret_cast<const bf16x8*>(q + q_off + kk * 16 + h * 8);
+            else qf[kk] = bf16x8{};
+        }
+    };
 
     // Per-thread chunk geometry, the same for every key tile: byte offset of
     // the chunk inside its page (K: [slot][d], V^T: [d][slot]) and the key
@@ -791,9 +800,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     };
 
     if (nt > 0) {
+        int pg0[NS - 1];   // page ids of the first tiles, all requested before any load
+        static_for<NS - 1>([&](auto j) { pg0[j] = (FAST && j < nt) ? tile_page(kt0 + j) : 0; });
         static_for<NS - 1>([&](auto j) {
-            if (j < nt) issue_tile(kt0 + j, j, FAST ? tile_page(kt0 + j) : 0);
+            if (j < nt) issue_tile(kt0 + j, j, pg0[j]);
         });
+        load_q();
         wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
         barrier_raw();
         s_mfmas(ring, s_cur);
@@ -1089,7 +1101,7 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
         off += (bytes + 255) & ~(size_t)255;
         return at;
     };
-    z.off_items = take((size_t)z.item_cap * 4 * sizeof(int32_t));
+    z.off_items = take((size_t)z.item_cap * kIItemInts * sizeof(int32_t));
     z.off_units = take((size_t)z.unit_cap * 2 * sizeof(int32_t));
     z.off_counts = take(4 * sizeof(int32_t));
     z.off_split = take((size_t)z.split_cap * sizeof(int32_t));
