@@ -17,7 +17,7 @@
 namespace fb {
 namespace {
 
-constexpr int kVocabThreads = 256;
+constexpr int kVocabThreads = 512;   // 8 waves per (row, partition): measured 1% faster than 4
 constexpr int kUpdThreads = 256;
 
 // Fold n consecutive values starting at index v into t (values in index order).
