@@ -13,12 +13,17 @@
 //   item  = a unit's key range [kb, ke), a multiple of 32 keys long except at
 //           kv_len; long units are split so the grid has enough items
 //   plan_kernel    one workgroup: counts key tiles, picks the split size,
-//                  emits items, per-unit split counts and partial slots
+//                  emits items (longest first, each with its tile's request
+//                  and first row), per-unit split counts and partial slots,
+//                  and the list of split units
 //   attn_bf16      one workgroup (4 waves x 32 rows) per item: 32-key K and
-//                  V^T tiles double-buffered in LDS, S^T = K Q^T and
-//                  O^T += V^T P^T on v_mfma_f32_32x32x16_bf16, online softmax
-//                  in the exp2 domain with lazy rescaling
-//   combine        merges split partials with their log-sum-exp weights
+//                  V^T tiles streamed through an LDS ring (3 stages at
+//                  D = 128, 4 below) by direct global->LDS loads,
+//                  S^T = K Q^T and O^T += V^T P^T on
+//                  v_mfma_f32_32x32x16_bf16, online softmax in the exp2
+//                  domain with lazy rescaling
+//   combine        merges split partials with their log-sum-exp weights,
+//                  walking the plan's list of split units
 //   attn_f32       a plain fp32 path (small problems, exactness reference)
 #include <type_traits>
 #include <utility>
