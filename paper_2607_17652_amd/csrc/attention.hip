@@ -576,13 +576,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                 if (kg < ke && !ok) record_error(pv.hdr, b, FB_DERR_PAGE);
                 const unsigned char* src = reinterpret_cast<const unsigned char*>(k_cache);
                 if (ok) {
-                    const size_t inpage = (size_t)(kg & (ps - 1)) - (size_t)ch_key[j] % ps;
+                    // ch_off addresses the chunk as if its tile began at slot
+                    // 0 of a page; move it to key kg's slot of its page
+                    const ptrdiff_t shift = (ptrdiff_t)(kg & (ps - 1)) - ch_key[j];
                     const uint16_t* base =
-                        ch_isk[j] ? k_cache + (size_t)page * page_elems + k_head + (size_t)(kg & (ps - 1)) * D -
-                                        (size_t)ch_key[j] * D
-                                  : v_cache + (size_t)page * page_elems + v_head + (kg & (ps - 1)) -
-                                        ch_key[j];
-                    (void)inpage;
+                        ch_isk[j] ? k_cache + (size_t)page * page_elems + k_head + shift * D
+                                  : v_cache + (size_t)page * page_elems + v_head + shift;
                     src = reinterpret_cast<const unsigned char*>(base) + ch_off[j];
                 }
                 const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
