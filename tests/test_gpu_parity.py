@@ -59,6 +59,13 @@ def test_longest_prefix_hits_the_split_cap():
     run_and_compare("single", prefix=("fixed", 65536), window=("fixed", 2), W_max=2)
 
 
+def test_more_tiles_than_the_plan_keeps_in_registers():
+    """1280 live tiles (320 requests x 4 blocks): the plan reads the fields
+    of the tiles beyond its register cache (1024) again from memory."""
+    run_and_compare("serve256", reqs=[0, 97, 191, 255, 256, 319], B=320,
+                    prefix=("loguniform", 64, 1024), window=("fixed", 4))
+
+
 def test_serve256_sampled_requests():
     rng = np.random.default_rng(7)
     reqs = sorted(rng.choice(256, size=12, replace=False).tolist())
