@@ -78,6 +78,8 @@ def test_serve256_sampled_requests():
     dict(page_size=64),
     dict(d=64, Hq=8, Hkv=8),                        # no GQA
     dict(d=32, Hq=16, Hkv=2),                       # group of 8
+    dict(d=64, Hq=8, Hkv=8, page_size=16),          # d = 64 with pages smaller than a key tile
+    dict(d=32, Hq=16, Hkv=2, page_size=8, prefix_jitter=11),   # d = 32, pages of 8
     dict(bl=16, page_size=16, W_max=5, window=("fixed", 5)),
     dict(bl=64, page_size=64, W_max=4, window=("uniform", 1, 4)),   # Table 2 lengths
     dict(bl=96, page_size=32, W_max=3, window=("fixed", 3)),        # bl not a power of 2
