@@ -163,6 +163,7 @@ __device__ int wg_excl_scan(int v, int* lds, int* total) {
 // first kPlanCache tiles are read once and kept in registers.
 constexpr int kLenBuckets = kPlanThreads;
 constexpr int kPlanCache = 4;
+constexpr int kPlanPieces = 1024;   // pieces of one round staged in LDS
 
 struct PlanTile {
     int kt;   // key tiles of the tile; 0 (skipped, error) past the page table
@@ -293,6 +294,14 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         __syncthreads();
     }
 
+    // A round's pieces are staged in LDS, then their items (a piece's
+    // per_tile items are contiguous) and the round's units are written by
+    // consecutive threads to consecutive entries, so the stores coalesce;
+    // a round with more pieces than the stage holds writes its items from
+    // the owning thread instead.
+    __shared__ int4 s_pc[kPlanPieces];   // per piece: first item, kb, ke, slot base (or -1)
+    __shared__ int4 s_pt[kPlanPieces];   // per piece: tile, splits of the tile, request, first row
+    __shared__ int4 s_tl[kPlanThreads];  // per tile of the round: splits, first slot, first split entry
     int items_before = 0, slots_before = 0, split_before = 0;
     for (int c = 0; c < n_rounds; ++c) {
         const int t = c * kPlanThreads + threadIdx.x;
@@ -304,31 +313,56 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         int ex[3] = {ns * per_tile, ns > 1 ? ns * per_tile : 0, ns > 1 ? per_tile : 0};
         int tot[3];
         wg_excl_scan3(ex, tot, trio_lds);
-        const int slot_t = slots_before + ex[1];
-        const int split_t = split_before + ex[2];
+        const int slot_t = slots_before + ex[1];     // unit j owns slots slot_t + j*ns ..
+        const int split_t = split_before + ex[2];    // and, when split, list entry split_t + j
+        const int piece0 = ex[0] / per_tile;         // this tile's first piece in the round
+        const int round_pieces = tot[0] / per_tile;
+        const bool staged = round_pieces <= kPlanPieces;
+        s_tl[threadIdx.x] = make_int4(ns, slot_t, split_t, 0);
         if (t < n_tiles) {
-            // unit j of the tile owns slots slot_t + j*ns .. + ns-1 and, when
-            // split, entry split_t + j of the list the merge walks
-            for (int j = 0; j < per_tile; ++j) {
-                const int u = t * per_tile + j;
-                ws.units[(size_t)u * 2 + kUSplits] = ns;
-                ws.units[(size_t)u * 2 + kUSlot0] = ns > 1 ? slot_t + j * ns : -1;
-                if (ns > 1 && split_t + j < split_cap) ws.split[split_t + j] = u;
-            }
             for (int k = 0; k < ns; ++k) {
                 const int pos = atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
                 const long long kb = (long long)k * chunk * kKeyTile;
                 long long ke = k == ns - 1 ? (long long)p.kv : kb + (long long)chunk * kKeyTile;
                 if (ke > p.kv) ke = p.kv;
-                for (int j = 0; j < per_tile; ++j) {
-                    if (pos + j >= item_cap) break;   // cannot happen: the loop above fits the caps
-                    int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(pos + j) * kIItemInts);
-                    it[0] = make_int4(t * per_tile + j, (int)kb, (int)ke,
-                                      ns > 1 ? slot_t + j * ns + k : -1);
-                    it[1] = make_int4(p.b, p.row0, 0, 0);
+                const int slot_k = ns > 1 ? slot_t + k : -1;
+                if (staged) {
+                    s_pc[piece0 + k] = make_int4(pos, (int)kb, (int)ke, slot_k);
+                    s_pt[piece0 + k] = make_int4(t, ns, p.b, p.row0);
+                } else {
+                    for (int j = 0; j < per_tile; ++j) {
+                        if (pos + j >= item_cap) break;   // cannot happen: the caps hold
+                        int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(pos + j) * kIItemInts);
+                        it[0] = make_int4(t * per_tile + j, (int)kb, (int)ke,
+                                          slot_k < 0 ? -1 : slot_k + j * ns);
+                        it[1] = make_int4(p.b, p.row0, 0, 0);
+                    }
                 }
             }
         }
+        __syncthreads();
+        int round_tiles = n_tiles - c * kPlanThreads;
+        if (round_tiles > kPlanThreads) round_tiles = kPlanThreads;
+        for (int e = threadIdx.x; e < round_tiles * per_tile; e += kPlanThreads) {
+            const int tl = e / per_tile, j = e % per_tile;
+            const int4 q = s_tl[tl];
+            const int u = (c * kPlanThreads + tl) * per_tile + j;
+            ws.units[(size_t)u * 2 + kUSplits] = q.x;
+            ws.units[(size_t)u * 2 + kUSlot0] = q.x > 1 ? q.y + j * q.x : -1;
+            if (q.x > 1 && q.z + j < split_cap) ws.split[q.z + j] = u;
+        }
+        if (staged) {
+            for (int e = threadIdx.x; e < round_pieces * per_tile; e += kPlanThreads) {
+                const int pc = e / per_tile, j = e % per_tile;
+                const int4 a = s_pc[pc];
+                const int4 m = s_pt[pc];
+                if (a.x + j >= item_cap) continue;   // cannot happen: the caps hold
+                int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(a.x + j) * kIItemInts);
+                it[0] = make_int4(m.x * per_tile + j, a.y, a.z, a.w < 0 ? -1 : a.w + j * m.y);
+                it[1] = make_int4(m.z, m.w, 0, 0);
+            }
+        }
+        __syncthreads();   // the stage is reused by the next round
         items_before += tot[0];
         slots_before += tot[1];
         split_before += tot[2];
