@@ -160,7 +160,7 @@ __device__ int wg_excl_scan(int v, int* lds, int* total) {
 // have the same key range, so they get the same split and adjacent items
 // (with 8 kv-heads the round-robin dispatch then keeps each kv-head on one
 // XCD).  Thread i handles tiles i, i + kPlanThreads, ...; the fields of its
-// first kPlanCache tiles are read once and kept in registers.
+// first kPlanCache tiles are read once and kept in LDS.
 constexpr int kLenBuckets = kPlanThreads;
 constexpr int kPlanCache = 4;
 constexpr int kPlanPieces = 1024;   // pieces of one round staged in LDS
@@ -203,19 +203,18 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     const int n_units = n_tiles * per_tile;
     const int n_rounds = (n_tiles + kPlanThreads - 1) / kPlanThreads;
 
-    PlanTile cache[kPlanCache];
+    // this thread's first kPlanCache tiles, read once; kept in LDS (a
+    // register array indexed by the round would live in scratch memory)
+    __shared__ PlanTile s_cache[kPlanCache * kPlanThreads];
 #pragma unroll
     for (int j = 0; j < kPlanCache; ++j)
-        cache[j] = plan_tile(pv.tiles, j * kPlanThreads + threadIdx.x, n_tiles, max_keys);
+        s_cache[j * kPlanThreads + threadIdx.x] =
+            plan_tile(pv.tiles, j * kPlanThreads + threadIdx.x, n_tiles, max_keys);
     // this thread's tile of round c (zeros past the end)
     auto tile_of = [&](int c) -> PlanTile {
         if (c >= kPlanCache)
             return plan_tile(pv.tiles, c * kPlanThreads + threadIdx.x, n_tiles, max_keys);
-        PlanTile p = cache[0];
-#pragma unroll
-        for (int j = 1; j < kPlanCache; ++j)
-            if (c == j) p = cache[j];
-        return p;
+        return s_cache[c * kPlanThreads + threadIdx.x];
     };
 
     // key tiles summed over the tiles, and the longest tile
@@ -302,6 +301,12 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     __shared__ int4 s_pc[kPlanPieces];   // per piece: first item, kb, ke, slot base (or -1)
     __shared__ int4 s_pt[kPlanPieces];   // per piece: tile, splits of the tile, request, first row
     __shared__ int4 s_tl[kPlanThreads];  // per tile of the round: splits, first slot, first split entry
+    // the entries a thread writes: unit / item j of every tpi-th tile or
+    // piece from my_tl on (no division per entry)
+    const int tpi = per_tile <= kPlanThreads ? kPlanThreads / per_tile : 1;
+    const int my_tl = per_tile <= kPlanThreads ? (int)threadIdx.x / per_tile : 0;
+    const int my_j = per_tile <= kPlanThreads ? (int)threadIdx.x % per_tile : 0;
+    const bool by_lane = per_tile <= kPlanThreads;
     int items_before = 0, slots_before = 0, split_before = 0;
     for (int c = 0; c < n_rounds; ++c) {
         const int t = c * kPlanThreads + threadIdx.x;
@@ -343,24 +348,33 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         __syncthreads();
         int round_tiles = n_tiles - c * kPlanThreads;
         if (round_tiles > kPlanThreads) round_tiles = kPlanThreads;
-        for (int e = threadIdx.x; e < round_tiles * per_tile; e += kPlanThreads) {
-            const int tl = e / per_tile, j = e % per_tile;
+        auto write_unit = [&](int tl, int j) {
             const int4 q = s_tl[tl];
             const int u = (c * kPlanThreads + tl) * per_tile + j;
             ws.units[(size_t)u * 2 + kUSplits] = q.x;
             ws.units[(size_t)u * 2 + kUSlot0] = q.x > 1 ? q.y + j * q.x : -1;
             if (q.x > 1 && q.z + j < split_cap) ws.split[q.z + j] = u;
-        }
-        if (staged) {
-            for (int e = threadIdx.x; e < round_pieces * per_tile; e += kPlanThreads) {
-                const int pc = e / per_tile, j = e % per_tile;
-                const int4 a = s_pc[pc];
-                const int4 m = s_pt[pc];
-                if (a.x + j >= item_cap) continue;   // cannot happen: the caps hold
-                int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(a.x + j) * kIItemInts);
-                it[0] = make_int4(m.x * per_tile + j, a.y, a.z, a.w < 0 ? -1 : a.w + j * m.y);
-                it[1] = make_int4(m.z, m.w, 0, 0);
+        };
+        auto write_item = [&](int pc, int j) {
+            const int4 a = s_pc[pc];
+            const int4 m = s_pt[pc];
+            if (a.x + j >= item_cap) return;   // cannot happen: the caps hold
+            int4* it = reinterpret_cast<int4*>(ws.items + (size_t)(a.x + j) * kIItemInts);
+            it[0] = make_int4(m.x * per_tile + j, a.y, a.z, a.w < 0 ? -1 : a.w + j * m.y);
+            it[1] = make_int4(m.z, m.w, 0, 0);
+        };
+        if (by_lane) {
+            if (my_tl < tpi) {
+                for (int tl = my_tl; tl < round_tiles; tl += tpi) write_unit(tl, my_j);
+                if (staged)
+                    for (int pc = my_tl; pc < round_pieces; pc += tpi) write_item(pc, my_j);
             }
+        } else {
+            for (int e = threadIdx.x; e < round_tiles * per_tile; e += kPlanThreads)
+                write_unit(e / per_tile, e % per_tile);
+            if (staged)
+                for (int e = threadIdx.x; e < round_pieces * per_tile; e += kPlanThreads)
+                    write_item(e / per_tile, e % per_tile);
         }
         __syncthreads();   // the stage is reused by the next round
         items_before += tot[0];
