@@ -90,13 +90,22 @@ struct VecTraits<float> {
 template <typename T>
 __global__ void __launch_bounds__(kVocabThreads)
 vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
-                  PackView pv, float4* __restrict__ part) {
+                  PackView pv, float4* __restrict__ part, int bl, int padded) {
     using VT = VecTraits<T>;
     constexpr int N = VT::N;
     constexpr int kBatch = 4;
-    const int row = blockIdx.x / nsplit;
+    const int slot = blockIdx.x / nsplit;
     const int k = blockIdx.x % nsplit;
-    if (pv.row_req[row] < 0) return;
+    int row = slot;
+    if (padded) {
+        // workgroups walk the live tiles' rows first, so the padding rows
+        // of the layout are not interleaved with live ones in the grid
+        const int t = slot / bl;
+        if (t >= pv.hdr[kHdrTiles]) return;
+        row = pv.tiles[(size_t)t * kTileInts + kTRow0] + slot % bl;
+    } else if (pv.row_req[row] < 0) {   // ragged rows are tile-major: live ones first
+        return;
+    }
     const int v0 = k * chunk;
     const int v1 = min(V, v0 + chunk);
     const T* rp = logits + (size_t)row * V;
@@ -517,11 +526,11 @@ hipError_t launch_vocab_reduce(const void* logits, int V, int dtype,
     if (dtype == FB_BF16) {
         hipLaunchKernelGGL(vocab_pass_kernel<uint16_t>, grid, dim3(kVocabThreads), 0,
                            stream, static_cast<const uint16_t*>(logits), V, z.nsplit,
-                           z.chunk, pv, part);
+                           z.chunk, pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
     } else {
         hipLaunchKernelGGL(vocab_pass_kernel<float>, grid, dim3(kVocabThreads), 0,
                            stream, static_cast<const float*>(logits), V, z.nsplit,
-                           z.chunk, pv, part);
+                           z.chunk, pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
     }
     return hipGetLastError();
 }
