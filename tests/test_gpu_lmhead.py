@@ -43,13 +43,15 @@ def oracle_rows(hid, weight, rows, chunk=16384):
     return dict(Z=Z, xhat=xhat, p=p, gap=m - second, bound=bound)
 
 
-def run_case(name, V, D, seed, sample=None, **overrides):
+def run_case(name, V, D, seed, sample=None, edit=None, **overrides):
     wl = synth.workload(name, V=V, **overrides)
     host = synth.make_host_state(wl, seed)
     log(f"[lmhead] {name} V={V} D={D} B={wl.B} rows={wl.row_cap}")
     t = synth.make_device_tensors(wl, host, seed, device="cuda", with_logits=False)
     step = WavefrontStep(wl, host, dict(t, logits=None))
     hid, weight = synth.make_lmhead_tensors(wl, D, seed)
+    if edit is not None:
+        edit(hid, weight)
     lm_ws = torch.empty(fb.fb_lmhead_workspace_bytes(step.pack, V, D), dtype=torch.uint8,
                         device="cuda")
     tokens_before = host["tokens"].copy()
@@ -87,6 +89,29 @@ def run_case(name, V, D, seed, sample=None, **overrides):
 ])
 def test_lmhead_reduce_matches_oracle(name, V, D, sample):
     run_case(name, V, D, seed=3, sample=sample)
+
+
+def test_lmhead_exact_ties_take_the_lowest_id():
+    """Seven vocabulary rows of W made equal to 256 e_0 and every hidden state
+    given h_0 = 1: each row's logits then hold seven exact maxima of 256 (one
+    nonzero product, so no rounding on either side) at ids in both lane halves,
+    both waves of a tile, other tiles and the last partition.  The argmax is the
+    lowest of them, 13, on every row."""
+    tied = [13, 14, 17, 45, 141, 269]
+
+    def edit(hid, weight):
+        V = weight.shape[0]
+        ids = torch.tensor(tied + [V - 1], device=weight.device)
+        hid[:, 0] = 1.0
+        weight[ids] = 0
+        weight[ids, 0] = 256.0
+
+    wl, host, packed, g, rows, o, tie, tok0 = run_case(
+        "hetero64", 157184, 256, seed=6, sample=96, edit=edit, B=16,
+        prefix=("uniform", 64, 512))
+    assert np.all(o["xhat"] == 13) and np.all(o["gap"] == 0)
+    assert np.all(g["argmax"][rows] == 13)
+    assert np.all(o["Z"][:, 13] == 256.0)
 
 
 def test_lmhead_reduce_then_update_matches_oracle_update():

@@ -290,6 +290,75 @@ def test_update_flags(flags):
     compare_case(wl, case, g, step, check_attention=False, check_kv=False)
 
 
+def _plant_ties(logits, V, seed):
+    """Exact ties at the row maximum, by row index mod 8: ids {0, V-1};
+    {V-2, V-1}; four random ids; two adjacent ids; two ids 4096 apart; a
+    constant row; no change; {x, V//2, V-1}.  Returns the lowest planted id
+    per row (-1 where nothing was planted)."""
+    rows = logits.shape[0]
+    rng = np.random.default_rng(seed)
+    m = logits.amax(dim=1).float()
+    tie = (m + torch.clamp(m.abs() / 16, min=1.0)).to(logits.dtype)
+    lowest = np.full(rows, -1, dtype=np.int64)
+    rr, ii, const = [], [], []
+    for r in range(rows):
+        kind = r % 8
+        if kind == 0:
+            ids = [0, V - 1]
+        elif kind == 1:
+            ids = [V - 2, V - 1]
+        elif kind == 2:
+            ids = rng.choice(V, size=4, replace=False).tolist()
+        elif kind == 3:
+            x = int(rng.integers(0, V - 1))
+            ids = [x, x + 1]
+        elif kind == 4:
+            x = int(rng.integers(0, V - 4096))
+            ids = [x, x + 4096]
+        elif kind == 5:
+            const.append(r)
+            lowest[r] = 0
+            continue
+        elif kind == 6:
+            continue
+        else:
+            ids = [int(rng.integers(0, V // 2)), V // 2, V - 1]
+        rr += [r] * len(ids)
+        ii += ids
+        lowest[r] = min(ids)
+    rr = torch.tensor(rr, device=logits.device)
+    logits[rr, torch.tensor(ii, device=logits.device)] = tie[rr]
+    logits[torch.tensor(const, device=logits.device)] = 0.25
+    return lowest
+
+
+@pytest.mark.parametrize("V", [157184, 5003])
+def test_argmax_ties_take_the_lowest_id(V):
+    """Exact ties at the maximum of a row (Eq. 1 takes the argmax; the
+    lowest id wins a tie) planted across the vocabulary partitions, inside
+    one 16-byte vector, a thread stride apart and over whole constant rows:
+    the GPU argmax equals the oracle's, which is the lowest planted id."""
+    wl, host, t, step = setup("hetero64", seed=12, V=V)
+    log(f"[parity] argmax ties V={V} rows={wl.row_cap}")
+    lowest = _plant_ties(t["logits"], V, seed=12)
+    case = OracleCase(wl, host, t, list(range(wl.B)), step.page_table)
+    step.run()
+    torch.cuda.synchronize()
+    g = gpu_results(step)
+    case.run(wl.params(), attention=False)
+    compare_case(wl, case, g, step, check_attention=False, check_kv=False)
+    n_planted = 0
+    for rf, rs in case.map_rows:
+        sel = lowest[rf] >= 0
+        assert np.array_equal(case.xhat[rs][sel], lowest[rf][sel])
+        assert np.array_equal(g["argmax"][rf][sel], lowest[rf][sel])
+        n_planted += int(sel.sum())
+    assert n_planted > 100
+    # a constant row has p = 1/V
+    const = [r for rf, _ in case.map_rows for r in rf if r % 8 == 5]
+    assert const and np.allclose(g["conf"][const], 1.0 / V, rtol=1e-6)
+
+
 @pytest.mark.parametrize("name", ["tiny", "single", "hetero64"])
 def test_multi_step_matches_oracle(name):
     """Four consecutive steps with fresh inputs each step: the GPU state and
