@@ -39,6 +39,9 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="serve256")
+    ap.add_argument("--second", default="long8",
+                    help="a second workload measured the same way and reported under "
+                         "its own key ('' to skip)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
@@ -133,13 +136,13 @@ def gather_kv(k_cache, v_cache, pt_row, T, ps):
 
 
 def cpu_baseline(wl, host, t, budget_s, seed):
-    """Time the fp64 oracle (as it stands) on whole requests, one at a time,
-    until the budget is spent; only the oracle's own computation is timed."""
+    """Time the fp64 oracle's whole step (as it stands) on whole requests, one
+    at a time, until the budget is spent; only the oracle's own computation is
+    timed (inputs are copied to host memory before the clock starts)."""
     import numpy as np
     import torch
-    from oracle import attention as oatt
     from oracle import pack as opack
-    from oracle import update as oupd
+    from oracle import step as ostep
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
@@ -176,25 +179,19 @@ def cpu_baseline(wl, host, t, budget_s, seed):
         tok = host["tokens"][[b]].copy()
         pe, fin = host["pe"][[b]].copy(), host["fin"][[b]].copy()
         t0 = time.perf_counter()
-        p2 = opack.pack_wavefronts(sub, wl.W_max, wl.bl, opack.RAGGED)
-        K2, V2 = oatt.write_window_kv([K], [V], kn, vn, p2)
-        oatt.window_attention(q, K2, V2, p2, wl.Hq, wl.Hkv)
-        live = np.flatnonzero(p2["row_req"] >= 0)
-        xhat = np.full(cap, -1, dtype=np.int64)
-        p64 = np.zeros(cap)
-        xhat[live], p64[live] = oupd.vocab_reduce(z[live])
-        oupd.denoise_update(xhat, p64, tok, sub, pe, fin, p2, params)
+        ostep.wavefront_step(sub, tok, pe, fin, q, kn, vn, [K], [V], z, params,
+                             wl.W_max, wl.bl, opack.RAGGED, wl.Hq, wl.Hkv)
         spent += time.perf_counter() - t0
-        rows_done += len(live)
+        rows_done += len(rs)
         reqs_done += 1
         if spent >= budget_s:
             break
     return {"value": rows_done / spent if spent > 0 else None, "unit": "tokens/s",
             "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"{reqs_done} of {wl.B} requests ({rows_done} live tokens): "
-                      f"pack, KV write, attention, vocab reduction, update in fp64 "
-                      f"numpy; {spent:.1f} s; matmuls on {blas_threads} BLAS "
-                      f"threads, the rest on one"}
+            "sample": f"{reqs_done} of {wl.B} requests ({rows_done} live tokens) of "
+                      f"{wl.name}: the oracle's whole step (pack, KV write, attention, "
+                      f"vocab reduction, update) in fp64 numpy; {spent:.1f} s; matmuls "
+                      f"on {blas_threads} BLAS threads, the rest on one"}
 
 
 def cold_steps(torch, one_step, step, K, nph, flush_bytes=1 << 30):
@@ -218,14 +215,16 @@ def cold_steps(torch, one_step, step, K, nph, flush_bytes=1 << 30):
             "steps": K, "flush_bytes": flush_bytes}
 
 
-def hbm_probe(torch, nbytes=2 << 30, reps=5):
-    """Measured device-memory rates to set the vocabulary pass against (besides
-    the 8 TB/s vendor figure): a plain device copy (bytes read + written per
-    second) and torch's sum over a bf16 tensor (bytes read per second), each
-    the best of `reps` launches timed with events."""
-    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+def hbm_probe(torch, fb, nbytes=2 << 30, reps=5):
+    """Measured device-memory ceilings beside the 8 TB/s vendor figure, from
+    the library's probes: a read-only stream with the vocabulary pass's load
+    form (bytes read per second) and a plain copy (bytes read + written per
+    second), each the best of `reps` launches timed with HIP events on the
+    launch stream.  The read probe's XOR result is checked against the
+    buffer's known contents."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(0x5a)
     dst = torch.empty_like(src)
-    xs = src.view(torch.bfloat16)
+    out = torch.empty(fb.FB_PROBE_BLOCKS, dtype=torch.int32, device="cuda")
 
     def best(fn):
         fn()
@@ -240,11 +239,18 @@ def hbm_probe(torch, nbytes=2 << 30, reps=5):
             ts.append(e0.elapsed_time(e1) * 1e-3)
         return min(ts)
 
-    t_copy = best(lambda: dst.copy_(src))
-    t_sum = best(lambda: xs.sum(dtype=torch.float32))
-    del src, dst, xs
-    return {"copy_GBps": 2 * nbytes / t_copy / 1e9, "sum_read_GBps": nbytes / t_sum / 1e9,
-            "bytes": nbytes, "note": "best of 5; copy counts bytes read + written"}
+    t_read = best(lambda: fb.fb_hbm_read_probe(src, out))
+    # every word is 0x5a5a5a5a and the buffer holds an even number of words,
+    # so the XOR of everything read is 0
+    xr = 0
+    for v in out.cpu().numpy().view("u4").tolist():
+        xr ^= v
+    t_copy = best(lambda: fb.fb_hbm_copy_probe(src, dst))
+    del src, dst
+    return {"read_GBps": nbytes / t_read / 1e9, "copy_GBps": 2 * nbytes / t_copy / 1e9,
+            "read_xor_ok": xr == 0, "bytes": nbytes,
+            "note": "library probes (fb_hbm_read_probe, fb_hbm_copy_probe), best of 5; "
+                    "copy counts bytes read + written"}
 
 
 def graph_replay(torch, fb, step, one_step, copies, K, W):
@@ -416,29 +422,17 @@ def loop_bench(torch, fb, synth, DecodeLoop):
             "hwp_over_sync": runs["hwp"]["tokens_per_s"] / runs["sync"]["tokens_per_s"]}
 
 
-def main():
-    args = parse_args()
-    if args.gpus != 1:
-        print(f"bench.py: the library runs one GPU per process; --gpus {args.gpus} is not "
-              f"supported here (requests are independent: each GPU would run this step on "
-              f"its own share of them)", file=sys.stderr)
-        sys.exit(2)
-    if args.copy_probe:
-        copy_probe()
-        return
+def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
+                 cold=True):
+    """K timed steps of one workload (after W warm-up steps), each on its own
+    copy of the pristine request state.  Returns (result dict, context for the
+    sections that reuse the step's buffers)."""
     import numpy as np
-    import torch
-    from paper_2607_17652_amd import binding as fb
-    from paper_2607_17652_amd import synth
-    from paper_2607_17652_amd.runner import DecodeLoop, WavefrontStep
-
-    torch.cuda.set_device(0)
-    wl = synth.workload(args.workload)
-    host = synth.make_host_state(wl, args.seed)
-    t = synth.make_device_tensors(wl, host, args.seed, device="cuda")
+    wl = synth.workload(name)
+    host = synth.make_host_state(wl, seed)
+    t = synth.make_device_tensors(wl, host, seed, device="cuda")
     step = WavefrontStep(wl, host, t)
     n_live, flops, attn_bytes = workload_work(wl, host)
-    K, W = args.steps, args.warmup
     copies = [(step.st.clone(), step.tokens.clone(), step.pe.clone(), step.fin.clone())
               for _ in range(K + W)]
     torch.cuda.synchronize()
@@ -489,8 +483,8 @@ def main():
                             for i in range(K)])) for j, n in enumerate(names)}
     ms_step = wall * 1e3 / K
     step_ms = [events[i][0].elapsed_time(events[i][nph]) for i in range(K)]
-    graph = None if args.no_graph else graph_replay(torch, fb, step, one_step, copies, K, W)
-    cold = None if args.no_cold else cold_steps(torch, one_step, step, K, nph)
+    gr = graph_replay(torch, fb, step, one_step, copies, K, W) if graph else None
+    cd = cold_steps(torch, one_step, step, K, nph) if cold else None
     t_attn = ph["attention"] * 1e-3
     t_voc = ph["vocab_reduce"] * 1e-3
     t_upd = (ph["vocab_reduce"] + ph["update_apply"]) * 1e-3
@@ -505,37 +499,68 @@ def main():
     roof_voc = {"kernel": "vocab_pass_kernel", "bound": "hbm",
                 "achieved": voc_ach / 1e9, "peak": PEAK_HBM_BYTES / 1e9,
                 "unit": "GB/s", "frac": voc_ach / PEAK_HBM_BYTES,
-                "traffic": voc_traffic}
+                "traffic": voc_traffic, "algorithmic_bytes": voc_bytes}
     roof_attn = {"kernel": "fb_wavefront_attention (plan+attn_bf16+combine)",
                  "bound": "mfma", "achieved": flops / t_attn / 1e12,
                  "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
                  "frac": attn_frac, "traffic": attn_traffic,
-                 "algorithmic_bytes": attn_bytes,
+                 "algorithmic_flops": flops, "algorithmic_bytes": attn_bytes,
                  "hbm_GBps_if_read_once": attn_bytes / t_attn / 1e9}
     dominant, other = (roof_voc, roof_attn) if t_voc >= t_attn else (roof_attn, roof_voc)
-    out = {
-        "metric": METRIC,
+    res = {
         "value": n_live / (ms_step * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms_step,
+        "ms_per_step": ms_step,
         "ms_per_step_median_events": float(np.median(step_ms)),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv,
                    "head_dim": wl.d, "bl": wl.bl, "W_max": wl.W_max,
                    "layout": wl.layout, "page_size": wl.page_size, "V": wl.V,
-                   "live_tokens": n_live, "seed": args.seed},
+                   "live_tokens": n_live, "seed": seed},
         "attn_pct_mfma_peak": 100.0 * attn_frac,
         "update_hbm_gbps": upd_bytes / t_upd / 1e9,
+        "update_pct_hbm_peak": 100.0 * upd_bytes / t_upd / PEAK_HBM_BYTES,
         "phases_ms": ph,
         "roofline": dominant,
         "roofline_other": other,
     }
-    if graph is not None:
-        out["graph"] = graph
-    if cold is not None:
-        out["cold"] = cold
-    out["hbm_probe"] = hbm_probe(torch)
+    if gr is not None:
+        res["graph"] = gr
+    if cd is not None:
+        res["cold"] = cd
+    del copies
+    ctx = dict(wl=wl, host=host, t=t, step=step, n_live=n_live)
+    return res, ctx
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: the library runs one GPU per process; --gpus {args.gpus} is not "
+              f"supported here (requests are independent: each GPU would run this step on "
+              f"its own share of them)", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
+    import torch
+    from paper_2607_17652_amd import binding as fb
+    from paper_2607_17652_amd import synth
+    from paper_2607_17652_amd.runner import DecodeLoop, WavefrontStep
+
+    torch.cuda.set_device(0)
+    K, W = args.steps, args.warmup
+    head, ctx = measure_step(torch, fb, synth, WavefrontStep, args.workload, args.seed,
+                             K, W, graph=not args.no_graph, cold=not args.no_cold)
+    wl, host, t, step, n_live = (ctx[k] for k in ("wl", "host", "t", "step", "n_live"))
+    out = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic",
+    }
+    out.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
+    out["hbm_probe"] = hbm_probe(torch, fb)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()
@@ -547,8 +572,15 @@ def main():
     if not args.no_lmhead:
         out["lmhead"] = lmhead_bench(torch, fb, synth, wl, step, t["logits"], n_live,
                                      args.lmhead_dim)
+    del ctx, step, t, host
+    torch.cuda.empty_cache()
+    if args.second and args.second != args.workload:
+        sec, sctx = measure_step(torch, fb, synth, WavefrontStep, args.second, args.seed,
+                                 K, W, graph=not args.no_graph, cold=not args.no_cold)
+        out[args.second] = sec
+        del sctx
+        torch.cuda.empty_cache()
     if not args.no_loop:
-        del copies
         out["loop"] = loop_bench(torch, fb, synth, DecodeLoop)
     print(json.dumps(out), flush=True)
 

@@ -78,8 +78,10 @@ extern "C" {
 
 /* ---- fb_update_params.flags ------------------------------------------- */
 #define FB_EDIT_MASKED    1u  /* literal Eq. 1: T2T may also overwrite [M]     */
-#define FB_FORCE_PROGRESS 2u  /* a block with masks but no M2T this step
-                                 unmasks its most confident masked row         */
+#define FB_FORCE_PROGRESS 2u  /* a block with masks none of which was
+                                 revealed this step (by Gamma, or by Delta
+                                 under FB_EDIT_MASKED) unmasks its most
+                                 confident masked row                          */
 #define FB_SYNC_WINDOW    4u  /* the batch-synchronous wavefront that the
                                  Sec. 5 ablation compares HWP with: every
                                  active request shares one window [L, R);
@@ -157,7 +159,8 @@ typedef struct fb_update_params {
     double   theta_spawn;  /* admission gate, Eq. 3 (>=)                       */
     int32_t  mask_id;      /* the [M] token id                                 */
     int32_t  eos_id;       /* < 0 disables the EOS stop                        */
-    int32_t  S_pe;         /* post-edit step cap (Sec. 3.1)                    */
+    int32_t  S_pe;         /* post-edit step cap (Sec. 3.1), 0..255 (pe is a
+                              uint8 counter that saturates at 255)             */
     int32_t  W;            /* admission cap, 1 <= W <= W_max of the pack       */
     uint32_t flags;        /* FB_EDIT_MASKED | FB_FORCE_PROGRESS |
                               FB_SYNC_WINDOW                                   */
@@ -308,7 +311,9 @@ size_t fb_update_workspace_bytes(const fb_pack* pack, int V);
  *  still stops only its own request), admit while the minimum of rho(B_{R-1})
  *  over them passes theta_spawn.  Active requests whose (L, R, n) differ are
  *  recorded as FB_DERR_STATE and no request retires or admits in that call.
- *   logits  [row_cap][V], dtype FB_BF16 or FB_F32; rows not live are not read
+ *   logits  [row_cap][V], dtype FB_BF16 or FB_F32; rows not live are not read;
+ *           a live row holds no NaN or +inf and at least one finite value
+ *           (-inf entries are allowed and weigh exp(-inf) = 0)
  *   tokens  int32[B][T_max], updated in place
  *   conf, argmax  [row_cap]; only live rows are written
  *   st      fb_req_state[B], updated in place
@@ -363,6 +368,25 @@ int fb_denoise_apply(int V, int32_t* tokens, int T_max, float* conf,
                      int n_max, const fb_pack* pack, const fb_update_params* prm,
                      fb_req_stats* stats, const void* ws, size_t ws_bytes,
                      void* stream);
+
+/* ---- Measured HBM ceilings ---------------------------------------------- */
+
+/* Workgroups of the probes: fb_hbm_read_probe writes one word per workgroup. */
+#define FB_PROBE_BLOCKS 2048
+
+/* Read-only stream over `bytes` of device memory at `src` with the load form
+ * of the vocabulary pass (16-byte nontemporal loads, four in flight per
+ * thread, a contiguous share per workgroup): the measured read ceiling the
+ * vocabulary reduction is set against.  out (device uint32[FB_PROBE_BLOCKS])
+ * receives, per workgroup, the XOR of the 32-bit words of its share; the XOR
+ * of all of them is the XOR of every word of the buffer.
+ *   src     16-byte aligned; bytes a positive multiple of 16 */
+int fb_hbm_read_probe(const void* src, size_t bytes, uint32_t* out, void* stream);
+
+/* Device copy of `bytes` from src to dst (16-byte loads and stores, the same
+ * shares): the measured read+write ceiling.  Both 16-byte aligned, not
+ * overlapping; bytes a positive multiple of 16. */
+int fb_hbm_copy_probe(const void* src, void* dst, size_t bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -17,25 +17,38 @@ from . import attention, pack, update
 
 
 def wavefront_step(state, tokens, pe, fin, q, k_new, v_new, K_prefix, V_prefix,
-                   logits, params, W_max, bl, layout, Hq, Hkv, sm_scale=None):
-    """All float inputs are float64 holding the exact values the GPU reads.
+                   logits, params, W_max, bl, layout, Hq, Hkv, sm_scale=None,
+                   with_attention=True):
+    """One whole step: pack (Eq. 4), window KV write (Eq. 6), block-causal
+    attention over the written caches (Sec. 4.1, Eq. 5), then the vocab
+    reduction and Alg. 1's update / retire / admit (Eq. 1-3).
 
-    logits: float64 [rows, V] in the packed layout (rows that are not live
-    may hold anything; they are not read).
-    Returns (packed, K, V, attn_out, update_result)."""
+    All float inputs are float64 holding the exact values the GPU reads;
+    q, k_new, v_new are in the packed row layout of ``layout``; K_prefix and
+    V_prefix are logical per-request caches [T_b, Hkv, d] (not modified).
+    logits: float64 [rows, V] in the packed layout, or a callable
+    ``logits(rows) -> float64 [len(rows), V]`` returning the given packed rows
+    (a large step need not hold every row at once; every row is reduced on
+    its own, so fetching rows in groups changes no value).  Rows that are not
+    live are never read.
+
+    Returns dict(packed, K, V, out (None without attention), xhat, p64,
+    update) with ``update`` the result of ``update.denoise_update``."""
     packed = pack.pack_wavefronts(state, W_max, bl, layout)
     K, V = attention.write_window_kv(K_prefix, V_prefix, k_new, v_new, packed)
-    out = attention.window_attention(q, K, V, packed, Hq, Hkv, sm_scale)
+    out = None
+    if with_attention:
+        out = attention.window_attention(q, K, V, packed, Hq, Hkv, sm_scale)
     live = np.flatnonzero(packed["row_req"] >= 0)
     xhat = np.full(packed["cap"], -1, dtype=np.int64)
     p64 = np.zeros(packed["cap"])
-    if live.size:
-        xh, pp = update.vocab_reduce(logits[live])
-        xhat[live] = xh
-        p64[live] = pp
+    for c0 in range(0, live.size, 128):
+        rows = live[c0:c0 + 128]
+        z = logits(rows) if callable(logits) else logits[rows]
+        xhat[rows], p64[rows] = update.vocab_reduce(z)
     res = update.denoise_update(xhat, p64, tokens, state, pe, fin, packed,
                                 params)
-    return packed, K, V, out, res
+    return dict(packed=packed, K=K, V=V, out=out, xhat=xhat, p64=p64, update=res)
 
 
 def gwd_loop(model, state, tokens, pe, fin, params, W_max, bl, layout,

@@ -92,7 +92,6 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
             g = t["g"]
             rows = range(t["row0"], t["row0"] + bl)
             x_old = {}
-            gamma = {}
             for r in rows:
                 pos = packed["row_pos"][r]
                 c32 = np.float32(p64[r])
@@ -108,7 +107,6 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
                 in_delta = ((edit_masked or not masked) and not prompt
                             and xhat[r] != x and _gt(c32, te)
                             and xhat[r] != mask_id)
-                gamma[r] = in_gamma
                 if in_gamma or in_delta:
                     tokens[b, pos] = xhat[r]
                     if masked:
@@ -116,9 +114,15 @@ def denoise_update(xhat, p64, tokens, state, pe, fin, packed, params):
                     else:
                         stats[b]["t2t"] += 1
             m_before = sum(1 for r in rows if x_old[r] == mask_id)
-            if force and m_before > 0 and not any(gamma.values()):
-                # Optional forced progress: unmask the most confident masked
-                # row (ties to the lowest position) whose prediction is not [M].
+            revealed = sum(1 for r in rows if x_old[r] == mask_id and
+                           int(tokens[b, packed["row_pos"][r]]) != mask_id)
+            if force and m_before > 0 and revealed == 0:
+                # Optional forced progress for a block where no masked row
+                # was revealed this step (neither by Gamma nor, under
+                # EDIT_MASKED, by Delta): unmask the most confident masked row
+                # (ties to the lowest position) whose prediction is not [M].
+                # Every masked row is then still masked, so none is counted
+                # twice.
                 best = None
                 for r in rows:
                     if x_old[r] == mask_id and xhat[r] != mask_id:

@@ -43,7 +43,9 @@ EXPORTS = [
     "fb_vocab_reduce", "fb_denoise_apply",
     "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
     "fb_lmhead_workspace_bytes", "fb_lmhead_reduce", "fb_window_prologue",
+    "fb_hbm_read_probe", "fb_hbm_copy_probe",
 ]
+FB_PROBE_BLOCKS = 2048
 
 
 class FlowBlockError(RuntimeError):
@@ -155,6 +157,8 @@ def lib():
                                       i32, i32, vp, vp, vp]),
             "fb_decode_loop": (i32, [P(fb_loop_args), i32, i32, i32, P(i32), P(i32),
                                      vp]),
+            "fb_hbm_read_probe": (i32, [vp, sz, vp, vp]),
+            "fb_hbm_copy_probe": (i32, [vp, vp, sz, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -401,3 +405,18 @@ def fb_decode_loop(args, max_steps, check_every, use_graph, stream=None):
                                 1 if use_graph else 0, ctypes.byref(steps),
                                 ctypes.byref(done), _stream(stream)))
     return steps.value, bool(done.value)
+
+
+# ------------------------------------------------------------- HBM probes
+def fb_hbm_read_probe(src, out, stream=None):
+    """Stream `src` (a contiguous device tensor) once; out: int32 or uint32
+    tensor of FB_PROBE_BLOCKS words receiving per-workgroup XORs."""
+    _check(lib().fb_hbm_read_probe(_ptr(src), src.numel() * src.element_size(),
+                                   _ptr(out), _stream(stream)))
+
+
+def fb_hbm_copy_probe(src, dst, stream=None):
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise FlowBlockError(FB_E_INVAL, "dst smaller than src")
+    _check(lib().fb_hbm_copy_probe(_ptr(src), _ptr(dst), nbytes, _stream(stream)))

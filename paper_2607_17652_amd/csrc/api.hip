@@ -256,7 +256,8 @@ int check_update_args(const fb_pack* pack, int V, const void* tokens, const void
     if (T_max < 1 || n_max < 1) return fail(FB_E_INVAL, "T_max and n_max must be >= 1");
     if (prm->W < 1 || prm->W > pack->W_max)
         return fail(FB_E_INVAL, "W %d outside [1, W_max=%d]", prm->W, pack->W_max);
-    if (prm->S_pe < 0) return fail(FB_E_INVAL, "S_pe must be >= 0");
+    if (prm->S_pe < 0 || prm->S_pe > 255)
+        return fail(FB_E_INVAL, "S_pe must be in [0, 255] (pe is a uint8 counter)");
     if (prm->mask_id < 0 || prm->mask_id >= V)
         return fail(FB_E_INVAL, "mask_id %d outside [0, V)", prm->mask_id);
     if (isnan(prm->tau_mask) || isnan(prm->tau_edit) || isnan(prm->theta_spawn))
@@ -598,6 +599,28 @@ int fb_decode_loop(const fb_loop_args* a, int max_steps, int check_every, int us
     cleanup();
     if (steps_out) *steps_out = enq;
     if (done_out) *done_out = done;
+    return ok();
+}
+
+int fb_hbm_read_probe(const void* src, size_t bytes, uint32_t* out, void* stream) {
+    if (!src || !out) return fail(FB_E_INVAL, "src and out must be device pointers");
+    if (!aligned16(src) || ((uintptr_t)out & 3u))
+        return fail(FB_E_INVAL, "src must be 16-byte and out 4-byte aligned");
+    if (bytes == 0 || bytes % 16) return fail(FB_E_INVAL, "bytes must be a positive multiple of 16");
+    hipError_t e = fb::launch_read_probe(src, bytes, out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "read probe launch");
+    return ok();
+}
+
+int fb_hbm_copy_probe(const void* src, void* dst, size_t bytes, void* stream) {
+    if (!src || !dst) return fail(FB_E_INVAL, "src and dst must be device pointers");
+    if (!aligned16(src) || !aligned16(dst)) return fail(FB_E_INVAL, "src and dst must be 16-byte aligned");
+    if (bytes == 0 || bytes % 16) return fail(FB_E_INVAL, "bytes must be a positive multiple of 16");
+    const char* a = static_cast<const char*>(src);
+    const char* b = static_cast<const char*>(dst);
+    if (a < b + bytes && b < a + bytes) return fail(FB_E_INVAL, "src and dst overlap");
+    hipError_t e = fb::launch_copy_probe(src, dst, bytes, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "copy probe launch");
     return ok();
 }
 

@@ -26,6 +26,9 @@ __device__ inline void top_fold(Top& t, const float (&f)[N], int v) {
     float vmax = f[0];
 #pragma unroll
     for (int j = 1; j < N; ++j) vmax = fmaxf(vmax, f[j]);
+    // A group of -inf logits adds exp(-inf) = 0.  Skipping it also keeps an
+    // empty running value (mL = -inf) away from the -inf + inf below.
+    if (vmax == -INFINITY) return;
     if (vmax > t.m) {
 #pragma clang fp contract(off)
         int j0 = N - 1;
@@ -176,7 +179,6 @@ struct UpdParams {
 enum RowFlag : uint8_t {
     kMaskedBefore = 1,
     kDecodable = 2,
-    kGamma = 4,
     kWritten = 8,
     kForceable = 16,
 };
@@ -239,7 +241,6 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         uint8_t f = 0;
         if (masked) f |= kMaskedBefore;
         if (masked && c >= prm.tau_mask) f |= kDecodable;
-        if (gamma) f |= kGamma;
         if (gamma || delta) {
             f |= kWritten;
             tok[pos] = xhat;
@@ -257,14 +258,13 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
     const int wave = tid >> 6;
     const int lane = tid & 63;
     for (int sl = wave; sl < w; sl += kUpdThreads / 64) {
-        int m_before = 0, dec = 0, n_gamma = 0, u = 0, wr_masked = 0;
+        int m_before = 0, dec = 0, u = 0, wr_masked = 0;
         float best_c = -1.f;
         int best_i = 0x7fffffff;
         for (int i = sl * bl + lane; i < (sl + 1) * bl; i += 64) {
             const uint8_t f = s_flag[i];
             m_before += (f & kMaskedBefore) ? 1 : 0;
             dec += (f & kDecodable) ? 1 : 0;
-            n_gamma += (f & kGamma) ? 1 : 0;
             u += (f & kWritten) ? 1 : 0;
             wr_masked += ((f & kWritten) && (f & kMaskedBefore)) ? 1 : 0;
             if ((f & kForceable) && s_conf[i] > best_c) {
@@ -276,7 +276,6 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         for (int off = 32; off > 0; off >>= 1) {
             m_before += __shfl_xor(m_before, off, 64);
             dec += __shfl_xor(dec, off, 64);
-            n_gamma += __shfl_xor(n_gamma, off, 64);
             u += __shfl_xor(u, off, 64);
             wr_masked += __shfl_xor(wr_masked, off, 64);
             const float oc = __shfl_xor(best_c, off, 64);
@@ -287,7 +286,10 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
             }
         }
         if (lane == 0) {
-            if ((prm.flags & FB_FORCE_PROGRESS) && m_before > 0 && n_gamma == 0 &&
+            // Forced progress only where no masked row was revealed (by
+            // Gamma, or by Delta under FB_EDIT_MASKED): every candidate is
+            // then still masked and no row is counted twice.
+            if ((prm.flags & FB_FORCE_PROGRESS) && m_before > 0 && wr_masked == 0 &&
                 best_i != 0x7fffffff) {
                 tok[o + best_i] = s_xhat[best_i];
                 u += 1;

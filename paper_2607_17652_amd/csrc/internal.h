@@ -123,6 +123,9 @@ hipError_t launch_synth_logits(const fb_req_state* st, const int32_t* tokens, in
                                int dtype, int32_t* pred, void* logits, hipStream_t stream);
 hipError_t launch_synth_embed(const fb_pack* pack, const fb_attn_shape* sh, uint64_t seed,
                               void* q, void* k_new, void* v_new, hipStream_t stream);
+hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* out,
+                             hipStream_t stream);
+hipError_t launch_copy_probe(const void* src, void* dst, size_t bytes, hipStream_t stream);
 hipError_t launch_loop_count(const fb_req_state* st, int B, fb_loop_counters* counters,
                              int32_t* forwards, int count, hipStream_t stream);
 

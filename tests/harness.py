@@ -10,15 +10,21 @@ import sys
 import numpy as np
 import torch
 
-from oracle import attention as oatt
 from oracle import pack as opack
-from oracle import update as oupd
+from oracle import step as ostep
 from paper_2607_17652_amd import binding as fb
 from paper_2607_17652_amd import synth
 from paper_2607_17652_amd.runner import WavefrontStep
 
 ATTN_TOL = {"bf16": 1e-2, "f32": 1e-5}
-CONF_TOL = 5e-6
+# Confidence: relative to the float64 value.  The kernel sums the row's
+# exponentials in float32 with at most about 60 roundings in sequence (up to
+# 40 groups of 8 per thread, the pairwise sum of a group, the wave and
+# workgroup merges, the partition merge and the final reciprocal), each
+# within 2^-24 relative on positive terms, plus one-ulp exp2 results: about
+# 4e-6 at worst; 5e-6 covers it.  The floor only matters for p near 1/V.
+CONF_RTOL = 5e-6
+CONF_ATOL = 1e-12
 
 
 def log(msg):
@@ -63,7 +69,8 @@ def rows_by_pos(packed, b):
 
 class OracleCase:
     """Oracle inputs for a subset `reqs` of a workload's requests, taken from
-    the generated tensors before the GPU step runs."""
+    the generated tensors before the GPU step runs (the live rows' logits are
+    copied to host memory then), and the oracle's whole step on them."""
 
     def __init__(self, wl, host, t, reqs, page_table):
         self.wl = wl
@@ -78,15 +85,23 @@ class OracleCase:
         self.k_new = np.zeros((cap, wl.Hkv, wl.d))
         self.v_new = np.zeros((cap, wl.Hkv, wl.d))
         self.map_rows = []          # (full rows, sub rows) per request
+        full_of_sub = np.full(cap, -1, dtype=np.int64)
         for i, b in enumerate(self.reqs):
             rf = rows_by_pos(self.full_packed, b)
             rs = rows_by_pos(self.sub_packed, i)
             self.map_rows.append((rf, rs))
+            full_of_sub[rs] = rf
             if len(rf):
                 idx = torch.from_numpy(rf).cuda()
                 self.q[rs] = t["q"][idx].double().cpu().numpy()
                 self.k_new[rs] = t["k_new"][idx].double().cpu().numpy()
                 self.v_new[rs] = t["v_new"][idx].double().cpu().numpy()
+        # the live rows' logits, in the sub pack's row order, kept in their
+        # own dtype on the host (widened to float64 a group at a time)
+        live = np.flatnonzero(full_of_sub >= 0)
+        self.logit_slot = np.full(cap, -1, dtype=np.int64)
+        self.logit_slot[live] = np.arange(live.size)
+        self.logits_host = t["logits"][torch.from_numpy(full_of_sub[live]).cuda()].cpu()
         self.T_need = []
         self.K_pre, self.V_pre = [], []
         for b in self.reqs:
@@ -103,27 +118,22 @@ class OracleCase:
         self.tokens = host["tokens"][self.reqs].copy()
         self.pe = host["pe"][self.reqs].copy()
         self.fin = host["fin"][self.reqs].copy()
-        # logits of the live rows -> (x_hat, p) by the oracle, in row chunks
-        self.xhat = np.full(cap, -1, dtype=np.int64)
-        self.p64 = np.zeros(cap)
-        for rf, rs in self.map_rows:
-            for c0 in range(0, len(rf), 128):
-                idx = torch.from_numpy(rf[c0:c0 + 128]).cuda()
-                z = t["logits"][idx].double().cpu().numpy()
-                xh, pp = oupd.vocab_reduce(z)
-                self.xhat[rs[c0:c0 + 128]] = xh
-                self.p64[rs[c0:c0 + 128]] = pp
+
+    def logits_rows(self, rows):
+        """float64 logits of sub-pack rows (all live)."""
+        slot = self.logit_slot[rows]
+        assert np.all(slot >= 0)
+        return self.logits_host[torch.from_numpy(slot)].double().numpy()
 
     def run(self, params, attention=True):
         wl = self.wl
-        self.K, self.V = oatt.write_window_kv(self.K_pre, self.V_pre, self.k_new,
-                                              self.v_new, self.sub_packed)
-        if attention:
-            self.out = oatt.window_attention(self.q, self.K, self.V,
-                                             self.sub_packed, wl.Hq, wl.Hkv)
-        self.upd = oupd.denoise_update(self.xhat, self.p64, self.tokens,
-                                       self.sub_state, self.pe, self.fin,
-                                       self.sub_packed, params)
+        r = ostep.wavefront_step(self.sub_state, self.tokens, self.pe, self.fin,
+                                 self.q, self.k_new, self.v_new, self.K_pre,
+                                 self.V_pre, self.logits_rows, params, wl.W_max,
+                                 wl.bl, opack.RAGGED, wl.Hq, wl.Hkv,
+                                 with_attention=attention)
+        self.K, self.V, self.out = r["K"], r["V"], r["out"]
+        self.xhat, self.p64, self.upd = r["xhat"], r["p64"], r["update"]
         return self
 
 
@@ -176,15 +186,19 @@ def compare_case(wl, case, g, step, check_attention=True, check_kv=True):
     upd = case.upd
     band_sub = set(upd["band_reqs"])
     summary = dict(attn_max_err=0.0, band_requests=[case.reqs[i] for i in band_sub],
-                   rows=0)
+                   rows=0, conf_max_rel=0.0)
     for i, b in enumerate(case.reqs):
         rf, rs = case.map_rows[i]
         summary["rows"] += len(rf)
         if len(rf):
             # vocab reduction: argmax exact, confidence to fp32 accuracy
             assert np.array_equal(g["argmax"][rf], upd["argmax"][rs]), f"argmax req {b}"
-            err = np.max(np.abs(g["conf"][rf].astype(np.float64) - case.p64[rs]))
-            assert err <= CONF_TOL, f"conf req {b}: {err}"
+            p64 = case.p64[rs]
+            err = np.abs(g["conf"][rf].astype(np.float64) - p64)
+            summary["conf_max_rel"] = max(summary["conf_max_rel"],
+                                          float(np.max(err / p64)))
+            assert np.all(err <= CONF_RTOL * p64 + CONF_ATOL), \
+                f"conf req {b}: max rel {np.max(err / p64):.3e}"
             if check_attention:
                 d = np.max(np.abs(step.out[torch.from_numpy(rf).cuda()].double()
                                   .cpu().numpy() - case.out[rs]))

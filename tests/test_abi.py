@@ -146,6 +146,17 @@ def test_calls_reject_bad_arguments_before_launch(lib):
                                fake, fake, 4, ctypes.byref(h), ctypes.byref(prm),
                                None, fake, 1 << 30, None)
     assert rc == fb.FB_E_INVAL
+    for S_pe in (-1, 256):                                     # pe is a uint8 count
+        prm = fb.make_params(0.9, 0.8, 0.5, 99, -1, S_pe, 2)
+        rc = lib.fb_denoise_update(fake, 100, fb.FB_BF16, fake, 64, fake, fake, fake,
+                                   fake, fake, 4, ctypes.byref(h), ctypes.byref(prm),
+                                   None, fake, 1 << 30, None)
+        assert rc == fb.FB_E_INVAL, S_pe
+        assert "S_pe" in fb.fb_last_error()
+        rc = lib.fb_denoise_apply(100, fake, 64, fake, fake, fake, fake, fake, 4,
+                                  ctypes.byref(h), ctypes.byref(prm), None, fake,
+                                  1 << 30, None)
+        assert rc == fb.FB_E_INVAL, S_pe
     prm = fb.make_params(0.9, 0.8, 0.5, 99, -1, 2, 2)
     prm.flags = 0x80
     rc = lib.fb_denoise_update(fake, 100, fb.FB_BF16, fake, 64, fake, fake, fake,
@@ -222,3 +233,15 @@ def test_loop_and_lmhead_calls_reject_bad_arguments_before_launch(lib):
     a.upd_ws_bytes = 16
     assert call(10, 4, 0) == fb.FB_E_WORKSPACE
     assert steps.value == -1 and done.value == -1               # nothing ran
+
+
+def test_probes_reject_bad_arguments_before_launch(lib):
+    fake = ctypes.c_void_p(0x10000)
+    other = ctypes.c_void_p(0x90000)
+    assert lib.fb_hbm_read_probe(None, 64, fake, None) == fb.FB_E_INVAL
+    assert lib.fb_hbm_read_probe(fake, 0, fake, None) == fb.FB_E_INVAL
+    assert lib.fb_hbm_read_probe(fake, 40, fake, None) == fb.FB_E_INVAL
+    assert lib.fb_hbm_read_probe(ctypes.c_void_p(0x10008), 64, fake, None) == fb.FB_E_INVAL
+    assert lib.fb_hbm_copy_probe(fake, ctypes.c_void_p(0x10010), 64, None) == fb.FB_E_INVAL
+    assert "overlap" in fb.fb_last_error()
+    assert lib.fb_hbm_copy_probe(fake, other, 24, None) == fb.FB_E_INVAL

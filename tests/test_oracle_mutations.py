@@ -27,6 +27,18 @@ MUTATIONS = [
      "sign error in the softmax normaliser"),
     ("update.py", "if u == 0 or pe[b, g] >= S_pe:", "if pe[b, g] >= S_pe:",
      "post-edit early stop dropped"),
+    ("update.py", "if force and m_before > 0 and revealed == 0:",
+     "if force and m_before > 0:",
+     "forced progress also where a masked row was revealed"),
+    ("step.py", "out = attention.window_attention(q, K, V, packed, Hq, Hkv, sm_scale)",
+     "out = attention.window_attention(q, K_prefix, V_prefix, packed, Hq, Hkv, sm_scale)",
+     "whole step attends over the caches before the window write"),
+    ("step.py", "xhat[rows], p64[rows] = update.vocab_reduce(z)",
+     "xhat[rows[::-1]], p64[rows[::-1]] = update.vocab_reduce(z)",
+     "whole step reduces the logits of the wrong rows"),
+    ("step.py", "res = update.denoise_update(xhat, p64, tokens, state, pe, fin, packed,\n                                params)\n    return dict(packed",
+     "res = update.denoise_update(xhat, p64, tokens, state, pe, fin, packed,\n                                dict(params, theta=1.0))\n    return dict(packed",
+     "whole step drops the caller's admission gate"),
     ("pack.py", "row0 = (next_ragged_block + s) * bl", "row0 = (b + s) * bl",
      "ragged rows overlap"),
     ("pack.py", "kv_len=o_b + (s + 1) * bl", "kv_len=o_b + s * bl",

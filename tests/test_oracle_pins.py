@@ -258,6 +258,88 @@ def test_attention_closed_forms():
     assert abs(wts.sum() - 1.0) < 1e-15
 
 
+# ------------------------------------------------------------ whole step ---
+@pytest.mark.parametrize("seed,layout", [(10, pack.RAGGED), (11, pack.PADDED)])
+def test_whole_step_attention_is_eq5_over_the_written_window(seed, layout):
+    """One whole step: the attention it returns is Eq. 5 applied literally on
+    the physical tail layout whose tail holds this step's fresh window K/V
+    (so the window's own keys must be visible, from the Eq. 6 write, not the
+    stale cache entries at those positions); the caches it returns hold the
+    window at o_b + delta and the old values everywhere else."""
+    rng = np.random.default_rng(seed)
+    c = make_case(rng, B=3, Hq=4, Hkv=2, d=8, bl=3, W_max=3, o_max=9)
+    Vv = 11
+    cap = c["B"] * c["W_max"] * c["bl"]
+    logits = rng.normal(size=(cap, Vv)) * 3
+    tokens = np.full((c["B"], int((c["o"] + c["state"]["n_blocks"] * c["bl"]).max())),
+                     Vv - 1, dtype=np.int64)
+    n_max = int(c["state"]["n_blocks"].max())
+    pe = np.zeros((c["B"], n_max), dtype=np.int64)
+    prm = dict(tau_mask=0.9, tau_edit=0.8, theta=0.5, mask_id=Vv - 1, eos_id=-1,
+               S_pe=2, W=c["W_max"])
+    res = step.wavefront_step(c["state"], tokens, pe, pe.copy(), c["q"], c["k_new"],
+                              c["v_new"], c["K"], c["V"], logits, prm, c["W_max"],
+                              c["bl"], layout, c["Hq"], c["Hkv"])
+    packed = res["packed"]
+    q_win, k_win, v_win = [], [], []
+    for b in range(c["B"]):
+        r = rows_of(packed, b)
+        q_win.append(c["q"][r])
+        k_win.append(c["k_new"][r])
+        v_win.append(c["v_new"][r])
+    bf = bruteforce.tail_layout_attention(q_win, c["K"], c["V"], k_win, v_win,
+                                          c["o"], c["w"], c["W_max"], c["bl"],
+                                          c["Hq"], c["Hkv"])
+    for b in range(c["B"]):
+        r = rows_of(packed, b)
+        assert np.max(np.abs(res["out"][r] - bf[b])) < 1e-12
+        o, n = int(c["o"][b]), int(c["w"][b]) * c["bl"]
+        assert np.array_equal(res["K"][b][o:o + n], k_win[b])
+        assert np.array_equal(res["V"][b][o:o + n], v_win[b])
+        assert np.array_equal(res["K"][b][:o], c["K"][b][:o])
+        assert np.array_equal(res["V"][b][o + n:], c["V"][b][o + n:])
+        # every live row's prediction is its own row's argmax
+        assert np.array_equal(res["xhat"][r], np.argmax(logits[r], axis=1))
+    # fetching rows through a callable gives the same step
+    res2 = step.wavefront_step(c["state"], tokens, pe, pe.copy(), c["q"], c["k_new"],
+                               c["v_new"], c["K"], c["V"], lambda rows: logits[rows],
+                               prm, c["W_max"], c["bl"], layout, c["Hq"], c["Hkv"])
+    assert np.array_equal(res2["out"], res["out"])
+    assert np.array_equal(res2["update"]["tokens"], res["update"]["tokens"])
+
+
+def test_whole_step_update_follows_the_first_hand_traced_step():
+    """Step 1 of the hand trace T1 (V = 5, bl = 2, W = 2; [M] = 4): logits
+    (4,1) at position 0 and (2,2) at position 1 reveal position 0 only
+    (p = .9317 > tau_mask; .6488 is not), rho(B0) = 1/2 >= theta admits B1.
+    Run as a whole step, with the logits given in the packed row layout."""
+    M_, bl, d = 4, 2, 2
+    state = dict(gen_start=np.array([0]), prompt_len=np.array([0]),
+                 n_blocks=np.array([3]), L=np.array([0]), R=np.array([1]),
+                 active=np.array([1]), eos_hit=np.array([0]))
+    tokens = np.full((1, 6), M_, dtype=np.int64)
+    pe = np.zeros((1, 3), dtype=np.int64)
+    cap = 2 * bl
+    logits = np.zeros((cap, 5))
+    logits[0, 1] = 4.0
+    logits[1, 2] = 2.0
+    logits[2:] = np.nan          # rows that are not live are never read
+    zq = np.zeros((cap, 1, d))
+    Kp = [np.zeros((6, 1, d))]
+    prm = dict(tau_mask=0.9, tau_edit=0.8, theta=0.5, mask_id=M_, eos_id=-1,
+               S_pe=1, W=2)
+    res = step.wavefront_step(state, tokens, pe, pe.copy(), zq, zq, zq, Kp, Kp,
+                              logits, prm, 2, bl, pack.RAGGED, 1, 1)
+    up = res["update"]
+    assert list(up["tokens"][0]) == [1, M_, M_, M_, M_, M_]
+    assert list(res["xhat"][:2]) == [1, 2]
+    assert abs(res["p64"][0] - 0.9317384593585715) < 1e-15
+    assert abs(res["p64"][1] - 0.6487856442839393) < 1e-15
+    assert (int(up["state"]["L"][0]), int(up["state"]["R"][0])) == (0, 2)
+    assert up["stats"][0]["m2t"] == 1 and up["stats"][0]["spawned"] == 1
+    assert up["stats"][0]["rho"] == 0.5
+
+
 # ------------------------------------------------------------ loop level ---
 def toy_model(V, bl_salt=0):
     """A deterministic stand-in for f_theta over a tiny vocabulary: the peak

@@ -228,6 +228,27 @@ def test_force_progress_flag():
     assert list(sim["tokens"][0][:2]) == [1, M]
 
 
+def test_force_progress_with_edit_masked_counts_each_row_once():
+    """With EDIT_MASKED and FORCE_PROGRESS, a masked row revealed by Delta
+    (tau_edit < p <= tau_mask) is this step's progress: nothing is forced.
+    pos0 (3,2): p = .834 > tau_edit, so Delta writes 2 (counted once, as
+    M2T, since the row was masked); pos1 (2,1): p = .649, stays [M].  With
+    S_pe = 0 the block still holds a mask, so it is not finished."""
+    sim = init([M] * 6)
+    prm = params(force_progress=True, edit_masked=True, S_pe=0)
+    r = step(sim, {0: (3, 2), 1: (2, 1)}, prm)
+    assert list(sim["tokens"][0][:2]) == [2, M]
+    assert r["stats"][0]["m2t"] == 1 and r["stats"][0]["t2t"] == 0
+    assert sim["fin"][0, 0] == 0
+    assert LR(sim) == (0, 1)        # rho(B0) = 0/2 < theta: no admission
+    # the same logits without EDIT_MASKED: no row is revealed, so the most
+    # confident masked row (pos0, p = .834) is forced
+    sim = init([M] * 6)
+    r = step(sim, {0: (3, 2), 1: (2, 1)}, params(force_progress=True, S_pe=0))
+    assert list(sim["tokens"][0][:2]) == [2, M]
+    assert r["stats"][0]["m2t"] == 1
+
+
 def test_multi_block_retire_in_one_step():
     """Finished blocks behind the leftmost retire together once the leftmost
     finishes (Alg. 1 inner while)."""
