@@ -369,6 +369,31 @@ int fb_denoise_apply(int V, int32_t* tokens, int T_max, float* conf,
                      fb_req_stats* stats, const void* ws, size_t ws_bytes,
                      void* stream);
 
+/* ---- The update without a caller workspace ------------------------------ */
+
+/* Bytes of the library's own update workspace, one per device. */
+#define FB_NOALLOC_SCRATCH_BYTES (4 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fb_denoise_update with the same arguments, results and errors, minus the
+ * workspace, which is a file-scope device array of FB_NOALLOC_SCRATCH_BYTES
+ * that each GPU the library runs on holds until the process ends.  Nothing
+ * is allocated or freed by the call (its address is looked up once per
+ * device, on the first call with that device current).
+ *   Limit: fb_update_workspace_bytes(pack, V) must not exceed
+ *   FB_NOALLOC_SCRATCH_BYTES (row_cap up to about 250K rows); above it the
+ *   call returns FB_E_UNSUPPORTED before enqueueing anything.
+ *   Every call on one GPU uses that GPU's one array: calls that overlap on
+ *   one GPU (different streams, or threads without ordering) race and give
+ *   undefined results.  Calls ordered on one stream are safe.  Nothing in the
+ *   array needs to start at zero: each call writes every value it reads. */
+int fb_denoise_update_noalloc(const void* logits, int V, int dtype, int32_t* tokens,
+                              int T_max, float* conf, int32_t* argmax, fb_req_state* st,
+                              uint8_t* pe, uint8_t* fin, int n_max, const fb_pack* pack,
+                              const fb_update_params* prm, fb_req_stats* stats,
+                              void* stream);
+
 /* ---- Measured HBM ceilings ---------------------------------------------- */
 
 /* Workgroups of the probes: fb_hbm_read_probe writes one word per workgroup. */

@@ -43,8 +43,9 @@ EXPORTS = [
     "fb_vocab_reduce", "fb_denoise_apply",
     "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
     "fb_lmhead_workspace_bytes", "fb_lmhead_reduce", "fb_window_prologue",
-    "fb_hbm_read_probe", "fb_hbm_copy_probe",
+    "fb_hbm_read_probe", "fb_hbm_copy_probe", "fb_denoise_update_noalloc",
 ]
+FB_NOALLOC_SCRATCH_BYTES = 4 << 20
 FB_PROBE_BLOCKS = 2048
 
 
@@ -158,6 +159,9 @@ def lib():
             "fb_decode_loop": (i32, [P(fb_loop_args), i32, i32, i32, P(i32), P(i32),
                                      vp]),
             "fb_hbm_read_probe": (i32, [vp, sz, vp, vp]),
+            "fb_denoise_update_noalloc": (i32, [vp, i32, i32, vp, i32, vp, vp, vp, vp,
+                                                vp, i32, P(fb_pack), P(fb_update_params),
+                                                vp, vp]),
             "fb_hbm_copy_probe": (i32, [vp, vp, sz, vp]),
         }
         for name, (res, args) in sig.items():
@@ -338,6 +342,18 @@ def fb_denoise_update(logits, tokens, conf, argmax, st, pe, fin, pack, params,
                                    _ptr(st), _ptr(pe), _ptr(fin), n_max,
                                    pack.ref(), ctypes.byref(params), _ptr(stats),
                                    _ptr(ws), nbytes, _stream(stream)))
+
+
+def fb_denoise_update_noalloc(logits, tokens, conf, argmax, st, pe, fin, pack, params,
+                              stats, stream=None):
+    """fb_denoise_update without a workspace argument: the library's own
+    per-device array serves as the workspace (nothing is allocated)."""
+    _check(lib().fb_denoise_update_noalloc(_ptr(logits), logits.shape[-1],
+                                           _dtype_code(logits), _ptr(tokens),
+                                           tokens.shape[-1], _ptr(conf), _ptr(argmax),
+                                           _ptr(st), _ptr(pe), _ptr(fin), pe.shape[-1],
+                                           pack.ref(), ctypes.byref(params), _ptr(stats),
+                                           _stream(stream)))
 
 
 def fb_vocab_reduce(logits, pack, ws, stream=None):

@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "internal.h"
 
 namespace {
@@ -374,6 +376,74 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens, int
     if (rc) return rc;
     const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
     rc = check_ws(ws, ws_bytes, z.total);
+    if (rc) return rc;
+    hipError_t e = fb::launch_vocab_reduce(logits, V, dtype, pack, ws, z,
+                                           (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "vocab reduction launch");
+    e = fb::launch_apply(tokens, T_max, conf, argmax, st, pe, fin, n_max, pack, prm, stats,
+                         ws, z, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "update launch");
+    return ok();
+}
+
+// ---- the update without a caller workspace -------------------------------
+}  // extern "C"
+
+// The update's workspace for callers that cannot allocate: one array per
+// device, alive until the process ends.  Host code never passes this name to
+// a kernel (on the host it is a stand-in, not a device address); it uses the
+// address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[FB_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // per device ordinal, guarded by g_scratch_mu
+
+// Device address of `scratch` on the current device, resolved once per
+// device (with that device current) and kept.
+int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(FB_E_UNSUPPORTED, "device ordinal %d above %d", dev, kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "resolving the update scratch array");
+        if (!p) return fail(FB_E_HIP, "the update scratch array has no device address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fb_denoise_update_noalloc(const void* logits, int V, int dtype, int32_t* tokens,
+                              int T_max, float* conf, int32_t* argmax, fb_req_state* st,
+                              uint8_t* pe, uint8_t* fin, int n_max, const fb_pack* pack,
+                              const fb_update_params* prm, fb_req_stats* stats,
+                              void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_reduce_args(pack, logits, V, dtype);
+    if (rc) return rc;
+    rc = check_update_args(pack, V, tokens, conf, argmax, st, pe, fin, prm, T_max, n_max);
+    if (rc) return rc;
+    const fb::UpdateSizes z = fb::update_sizes(pack, V, cu_count());
+    if (z.total > (size_t)FB_NOALLOC_SCRATCH_BYTES)
+        return fail(FB_E_UNSUPPORTED,
+                    "this pack and vocabulary need %zu bytes of update workspace, above "
+                    "the %d bytes fb_denoise_update_noalloc holds; use fb_denoise_update",
+                    z.total, FB_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    rc = scratch_address(&ws);
     if (rc) return rc;
     hipError_t e = fb::launch_vocab_reduce(logits, V, dtype, pack, ws, z,
                                            (hipStream_t)stream);

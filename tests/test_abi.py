@@ -245,3 +245,24 @@ def test_probes_reject_bad_arguments_before_launch(lib):
     assert lib.fb_hbm_copy_probe(fake, ctypes.c_void_p(0x10010), 64, None) == fb.FB_E_INVAL
     assert "overlap" in fb.fb_last_error()
     assert lib.fb_hbm_copy_probe(fake, other, 24, None) == fb.FB_E_INVAL
+
+
+def test_noalloc_update_rejects_a_pack_above_its_array(lib):
+    """fb_denoise_update_noalloc: a pack whose update workspace exceeds the
+    library's array is refused before anything is enqueued."""
+    fake = ctypes.c_void_p(0x10000)
+    B, W, bl = 8192, 4, 32                       # 2^20 rows of 16-byte partials
+    rc, h = _init(lib, fake, fb.fb_pack_bytes(B, W, bl), B, W, bl, fb.FB_RAGGED)
+    assert rc == fb.FB_OK
+    assert lib.fb_update_workspace_bytes(ctypes.byref(h), 157184) > fb.FB_NOALLOC_SCRATCH_BYTES
+    prm = fb.make_params(0.9, 0.8, 0.5, 157183, -1, 2, 4)
+    rc = lib.fb_denoise_update_noalloc(fake, 157184, fb.FB_BF16, fake, 4096, fake, fake,
+                                       fake, fake, fake, 64, ctypes.byref(h),
+                                       ctypes.byref(prm), None, None)
+    assert rc == fb.FB_E_UNSUPPORTED
+    assert "noalloc" in fb.fb_last_error()
+    prm.S_pe = 300                               # argument errors come first
+    rc = lib.fb_denoise_update_noalloc(fake, 157184, fb.FB_BF16, fake, 4096, fake, fake,
+                                       fake, fake, fake, 64, ctypes.byref(h),
+                                       ctypes.byref(prm), None, None)
+    assert rc == fb.FB_E_INVAL
