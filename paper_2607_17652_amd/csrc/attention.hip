@@ -951,21 +951,24 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 }
 
 // ------------------------------------------------------------ combine -----
+// Four consecutive output elements of one row.
 template <typename T>
-__device__ inline void store_out(T* p, float v);
+__device__ inline void store_out4(T* p, const float4& v);
 template <>
-__device__ inline void store_out<uint16_t>(uint16_t* p, float v) {
-    __bf16 x = (__bf16)v;
-    *p = *reinterpret_cast<uint16_t*>(&x);
+__device__ inline void store_out4<uint16_t>(uint16_t* p, const float4& v) {
+    __bf16 x[4] = {(__bf16)v.x, (__bf16)v.y, (__bf16)v.z, (__bf16)v.w};
+    *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(x);
 }
 template <>
-__device__ inline void store_out<float>(float* p, float v) { *p = v; }
+__device__ inline void store_out4<float>(float* p, const float4& v) {
+    *reinterpret_cast<float4*>(p) = v;
+}
 
 // Each split unit's rows are merged by kCombineParts workgroups of
 // kCombineRows rows (workgroup b takes entry b / kCombineParts of the plan's
 // list of split units, so the grid covers only units that can be split): a row's per-split log-sum-exp weights go to LDS once,
-// then every thread merges 16-byte columns of its rows, four splits' loads
-// in flight at a time.
+// then every thread merges 16-byte columns of its rows, up to eight splits'
+// loads in flight at a time.
 constexpr int kCombineRows = 32;
 constexpr int kCombineParts = kRowsPerWg / kCombineRows;
 
@@ -1015,27 +1018,24 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
             acc.z += w * v.z;
             acc.w += w * v.w;
         };
-        int k = 0;
-        for (; k + 4 <= ns; k += 4) {
-            const float4 v0 = *reinterpret_cast<const float4*>(src + (size_t)k * stride);
-            const float4 v1 = *reinterpret_cast<const float4*>(src + (size_t)(k + 1) * stride);
-            const float4 v2 = *reinterpret_cast<const float4*>(src + (size_t)(k + 2) * stride);
-            const float4 v3 = *reinterpret_cast<const float4*>(src + (size_t)(k + 3) * stride);
-            add(wgt[k][rr], v0);
-            add(wgt[k + 1][rr], v1);
-            add(wgt[k + 2][rr], v2);
-            add(wgt[k + 3][rr], v3);
+        // the splits' loads are issued eight at a time before any of them
+        // is used, so a unit of a few pieces waits for one round trip
+        constexpr int kInFlight = 8;
+        for (int k0 = 0; k0 < ns; k0 += kInFlight) {
+            float4 v[kInFlight];
+#pragma unroll
+            for (int j = 0; j < kInFlight; ++j)
+                if (k0 + j < ns)
+                    v[j] = *reinterpret_cast<const float4*>(src + (size_t)(k0 + j) * stride);
+#pragma unroll
+            for (int j = 0; j < kInFlight; ++j)
+                if (k0 + j < ns) add(wgt[k0 + j][rr], v[j]);
         }
-        for (; k < ns; ++k)
-            add(wgt[k][rr], *reinterpret_cast<const float4*>(src + (size_t)k * stride));
         const float id = inv_den[rr];
         const int r = rg * kRowsPerWg + rbase + rr;
         const int pos_local = r / g, hg = r % g;
         T* dst = out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d0;
-        store_out<T>(dst + 0, acc.x * id);
-        store_out<T>(dst + 1, acc.y * id);
-        store_out<T>(dst + 2, acc.z * id);
-        store_out<T>(dst + 3, acc.w * id);
+        store_out4<T>(dst, make_float4(acc.x * id, acc.y * id, acc.z * id, acc.w * id));
     }
 }
 
