@@ -132,24 +132,34 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
         for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
     Top top[2] = {top_empty(), top_empty()};
 
+    // The six fragments of k step kk + 1 are read while the eight MFMAs of k
+    // step kk issue, so an MFMA never waits on the read right before it.
     auto compute = [&](int stage) {
         const unsigned char* st = lds + stage * kStageBytes;
-#pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
+        constexpr int KK = kBK / 16;
+        bf16x8 a[2][4], b[2][2];
+        auto read = [&](int kk, int buf) {
             const uint32_t ko = swz ^ (uint32_t)(kk << 5);
-            bf16x8 a[4], b[2];
 #pragma unroll
             for (int vi = 0; vi < 4; ++vi)
-                a[vi] = *reinterpret_cast<const bf16x8*>(st + a_row + vi * 32 * kRowBytes + ko);
+                a[buf][vi] = *reinterpret_cast<const bf16x8*>(st + a_row + vi * 32 * kRowBytes + ko);
 #pragma unroll
             for (int ti = 0; ti < 2; ++ti)
-                b[ti] = *reinterpret_cast<const bf16x8*>(st + b_row + ti * 32 * kRowBytes + ko);
+                b[buf][ti] = *reinterpret_cast<const bf16x8*>(st + b_row + ti * 32 * kRowBytes + ko);
+        };
+        read(0, 0);
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const int cur = kk & 1;
+            if (kk + 1 < KK) read(kk + 1, cur ^ 1);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int vi = 0; vi < 4; ++vi)
 #pragma unroll
                 for (int ti = 0; ti < 2; ++ti)
-                    acc[vi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[vi], b[ti],
+                    acc[vi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][vi], b[cur][ti],
                                                                           acc[vi][ti], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
