@@ -470,24 +470,14 @@ def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
     for i in range(W):
         one_step(K + i, None)
     torch.cuda.synchronize()
-    # the timed steps record no events; the per-phase breakdown comes from a
-    # second pass of K steps on fresh state copies, each phase bracketed by
-    # HIP events on the launch stream
     t0 = time.perf_counter()
     for i in range(K):
-        one_step(i, None)
+        one_step(i, events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = fb.fb_pack_read_status(step.pack)
     if status["code"] != 0:
         raise RuntimeError(f"device status {status}")
-    phase_copies = [(step.st.clone(), step.tokens.clone(), step.pe.clone(), step.fin.clone())
-                    for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        one_step(i, events[i], phase_copies[i])
-    torch.cuda.synchronize()
-    del phase_copies
     names = ["pack", "kv_write", "attention", "vocab_reduce", "update_apply"]
     ph = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1])
                             for i in range(K)])) for j, n in enumerate(names)}
