@@ -1,8 +1,9 @@
 // Window KV write-back, Eq. 6 (Sec. 4.2, "KV retrieval and write-back"):
 // the fresh K/V of each live block lands at its absolute positions of the
-// paged caches.  One workgroup per (tile, KV head).  K rows are copied in
-// 16-byte vectors.  V is written key-innermost ([page][head][d][slot]): the
-// block's V rows are staged in LDS with 16-byte loads; when the block starts
+// paged caches.  One workgroup per (tile, KV head).  The block's K and V
+// rows are loaded first, in 16-byte vectors, and K is copied into its page
+// as the page ids arrive.  V is written key-innermost ([page][head][d][slot]):
+// the block's V rows are staged in LDS; when the block starts
 // on a 16-byte slot boundary each thread then gathers one 16-byte run of
 // slots for one d from LDS and stores it whole (neighbouring lanes fill
 // neighbouring runs of the same d row), otherwise element by element.
@@ -32,31 +33,54 @@ write_kv_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
     constexpr int VEC = 16 / sizeof(T);
     const int dch = D / VEC;
 
-    // K: straight 16-byte copies.
-    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
-        const int i = e / dch;
-        const int dc = e % dch;
-        const int pos = pos0 + i;
-        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
-        const int pidx = pos / ps;
-        const int page = pidx < max_pages ? pt[pidx] : -1;
-        if (page < 0 || page >= num_pages) {
-            if (dc == 0) record_error(pv.hdr, b, FB_DERR_PAGE);
-            continue;
+    // The window's K and V rows are loaded before any page id is known (their
+    // addresses do not depend on it), together with the page-table reads;
+    // a thread holds kBatch 16-byte chunks of each at a time.
+    constexpr int kBatch = 2;
+    const int n_ch = bl * dch;
+    for (int e0 = 0; e0 < n_ch; e0 += kBatch * kKvThreads) {
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        u32x4 kx[kBatch], vx[kBatch];
+        int pg[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            // past the block's last chunk a thread reloads that chunk (an
+            // address inside the block) and stores nothing below
+            const int e = min(e0 + j * kKvThreads + (int)threadIdx.x, n_ch - 1);
+            const int i = e / dch;
+            const int dc = e % dch;
+            const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
+            kx[j] = *reinterpret_cast<const u32x4*>(k_new + src);
+            vx[j] = *reinterpret_cast<const u32x4*>(v_new + src);
+            const int pidx = (pos0 + i) / ps;
+            const int p = pt[min(pidx, max_pages - 1)];
+            pg[j] = pidx < max_pages ? p : -1;
         }
-        const size_t dst = (((size_t)page * Hkv + c) * ps + (pos % ps)) * D +
-                           (size_t)dc * VEC;
-        *reinterpret_cast<uint4*>(k_cache + dst) =
-            *reinterpret_cast<const uint4*>(k_new + src);
-    }
-    // V: stage the block's V rows in LDS ([bl][pitch], 16-byte loads), then
-    // write the cache's key-innermost rows.
-    for (int e = threadIdx.x; e < bl * dch; e += kKvThreads) {
-        const int i = e / dch;
-        const int dc = e % dch;
-        const size_t src = ((size_t)(row0 + i) * Hkv + c) * D + (size_t)dc * VEC;
-        *reinterpret_cast<uint4*>(vs + (size_t)i * pitch + dc * VEC) =
-            *reinterpret_cast<const uint4*>(v_new + src);
+        // every load above is issued before any of them is waited for (the
+        // compiler would otherwise sink each load to its use)
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            asm volatile("" :: "v"(kx[j]), "v"(vx[j]), "v"(pg[j]));
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int e = e0 + j * kKvThreads + threadIdx.x;
+            if (e < n_ch) {
+                const int i = e / dch;
+                const int dc = e % dch;
+                // V: staged in LDS ([bl][pitch]) for the key-innermost writes below
+                *reinterpret_cast<u32x4*>(vs + (size_t)i * pitch + dc * VEC) = vx[j];
+                // K: straight 16-byte copy into the page
+                const int pos = pos0 + i;
+                const int page = pg[j];
+                if (page >= 0 && page < num_pages) {
+                    const size_t dst = (((size_t)page * Hkv + c) * ps + (pos % ps)) * D +
+                                       (size_t)dc * VEC;
+                    *reinterpret_cast<u32x4*>(k_cache + dst) = kx[j];
+                } else if (dc == 0) {
+                    record_error(pv.hdr, b, FB_DERR_PAGE);
+                }
+            }
+        }
     }
     __syncthreads();
     if (pos0 % VEC == 0 && ps % VEC == 0 && bl % VEC == 0) {
