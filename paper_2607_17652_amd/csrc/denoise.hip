@@ -200,7 +200,10 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
 
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
+    // the request's fields are read together (each is in bounds for any b)
     const int w = pv.req_w[b];
+    const fb_req_state s = st[b];
+    const int row0 = pv.req_row0[b];
     if (w < 0) {
         if (tid == 0 && stats) {
             fb_req_stats z{};
@@ -210,8 +213,6 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         }
         return;
     }
-    const fb_req_state s = st[b];
-    const int row0 = pv.req_row0[b];
     const int nrows = w * bl;
     const int o = s.gen_start + s.L * bl;
     int32_t* tok = tokens + (size_t)b * T_max;
@@ -221,9 +222,24 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         const int row = row0 + i;
         const int pos = o + i;
         const float4* pr = part + (size_t)row * nsplit;
-        float4 p0 = pr[0];
-        Top t{p0.x, p0.w, p0.y, __float_as_int(p0.z)};
-        for (int k = 1; k < nsplit; ++k) {
+        // the row's token and its first partials are loaded together before
+        // any is used (merged below in partition order, as before)
+        constexpr int kPre = 4;
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        f32x4 pre[kPre];
+#pragma unroll
+        for (int k = 0; k < kPre; ++k)
+            pre[k] = *reinterpret_cast<const f32x4*>(pr + (k < nsplit ? k : nsplit - 1));
+        const int x = tok[pos];
+#pragma unroll
+        for (int k = 0; k < kPre; ++k) asm volatile("" :: "v"(pre[k]));
+        asm volatile("" :: "v"(x));
+        Top t{pre[0][0], pre[0][3], pre[0][1], __float_as_int(pre[0][2])};
+#pragma unroll
+        for (int k = 1; k < kPre; ++k)
+            if (k < nsplit)
+                t = top_merge(t, Top{pre[k][0], pre[k][3], pre[k][1], __float_as_int(pre[k][2])});
+        for (int k = kPre; k < nsplit; ++k) {
             const float4 pk = pr[k];
             t = top_merge(t, Top{pk.x, pk.w, pk.y, __float_as_int(pk.z)});
         }
@@ -231,7 +247,6 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
         const float resid = fmaf(t.m, kLog2e, -t.mL);
         const float conf = 1.0f / (t.s * __builtin_amdgcn_exp2f(-resid));
         const int xhat = t.idx;
-        const int x = tok[pos];
         const bool masked = x == prm.mask_id;
         const bool prompt = pos < s.prompt_len;
         const double c = (double)conf;
