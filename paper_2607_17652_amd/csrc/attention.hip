@@ -56,7 +56,8 @@ struct AttnWs {
     int32_t* items;    // [item_cap][kIItemInts]
     int32_t* units;    // [unit_cap][2]
     int32_t* counts;   // [4]
-    int32_t* split;    // [split_cap]: the units with more than one piece
+    int4* split;       // [split_cap]: {unit, pieces, first slot, first row} of the
+                       // units with more than one piece
     float* part_o;     // [slot_cap][128][D]
     float* part_lse;   // [slot_cap][128]
 };
@@ -300,7 +301,8 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
     // the owning thread instead.
     __shared__ int4 s_pc[kPlanPieces];   // per piece: first item, kb, ke, slot base (or -1)
     __shared__ int4 s_pt[kPlanPieces];   // per piece: tile, splits of the tile, request, first row
-    __shared__ int4 s_tl[kPlanThreads];  // per tile of the round: splits, first slot, first split entry
+    __shared__ int4 s_tl[kPlanThreads];  // per tile of the round: splits, first slot, first
+                                         // split entry, first row
     // the entries a thread writes: unit / item j of every tpi-th tile or
     // piece from my_tl on (no division per entry)
     const int tpi = per_tile <= kPlanThreads ? kPlanThreads / per_tile : 1;
@@ -323,7 +325,7 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
         const int piece0 = ex[0] / per_tile;         // this tile's first piece in the round
         const int round_pieces = tot[0] / per_tile;
         const bool staged = round_pieces <= kPlanPieces;
-        s_tl[threadIdx.x] = make_int4(ns, slot_t, split_t, 0);
+        s_tl[threadIdx.x] = make_int4(ns, slot_t, split_t, p.row0);
         if (t < n_tiles) {
             for (int k = 0; k < ns; ++k) {
                 const int pos = atomicAdd(&bucket[len_key(p.kr, k)], per_tile);
@@ -353,7 +355,8 @@ plan_kernel(PackView pv, AttnWs ws, int Hkv, int RG, int item_cap, int slot_cap,
             const int u = (c * kPlanThreads + tl) * per_tile + j;
             ws.units[(size_t)u * 2 + kUSplits] = q.x;
             ws.units[(size_t)u * 2 + kUSlot0] = q.x > 1 ? q.y + j * q.x : -1;
-            if (q.x > 1 && q.z + j < split_cap) ws.split[q.z + j] = u;
+            if (q.x > 1 && q.z + j < split_cap)
+                ws.split[q.z + j] = make_int4(u, q.x, q.y + j * q.x, q.w);
         };
         auto write_item = [&](int pc, int j) {
             const int4 a = s_pc[pc];
@@ -981,17 +984,38 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
     const int su = blockIdx.x / kCombineParts;
     const int part = blockIdx.x % kCombineParts;
     if (su >= ws.counts[kCSplit]) return;
-    const int u = ws.split[su];
-    const int ns = ws.units[(size_t)u * 2 + kUSplits];   // 2 .. kMaxSplits (plan)
+    // the plan's record of this split unit: no further lookups before the loads
+    const int4 rec = ws.split[su];
+    const int u = rec.x;
+    const int ns = rec.y;   // 2 .. kMaxSplits (plan)
     if (ns <= 1) return;
-    const int slot0 = ws.units[(size_t)u * 2 + kUSlot0];
+    const int slot0 = rec.z;
+    const int row0 = rec.w;
     const int rg = u % RG;
     const int c = (u / RG) % Hkv;
-    const int t = u / (RG * Hkv);
-    const int row0 = pv.tiles[(size_t)t * kTileInts + kTRow0];
     const int rbase = part * kCombineRows;
     const int nrows = min(kCombineRows, bl * g - rg * kRowsPerWg - rbase);
     if (nrows <= 0) return;
+    const int per_row = D / 4;
+    const int n_el = nrows * per_row;
+    const size_t stride = (size_t)kRowsPerWg * D;   // one split's partial O
+    auto src_of = [&](int e) {
+        return ws.part_o + ((size_t)slot0 * kRowsPerWg + rbase + e / per_row) * D +
+               (e % per_row) * 4;
+    };
+    // A thread's first column group: its splits' loads (up to eight) are
+    // issued before the weights below are ready, so they overlap.
+    constexpr int kInFlight = 8;
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4 first[kInFlight];
+    {
+        const float* src = src_of(min((int)threadIdx.x, n_el - 1));
+#pragma unroll
+        for (int j = 0; j < kInFlight; ++j)   // past the last split: reload it, unused
+            first[j] = *reinterpret_cast<const f32x4*>(src + (size_t)min(j, ns - 1) * stride);
+#pragma unroll
+        for (int j = 0; j < kInFlight; ++j) asm volatile("" :: "v"(first[j]));
+    }
     if (threadIdx.x < nrows) {
         const float* lse = ws.part_lse + (size_t)slot0 * kRowsPerWg + rbase + threadIdx.x;
         float mx = -INFINITY;
@@ -1005,28 +1029,30 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
         inv_den[threadIdx.x] = 1.0f / den;
     }
     __syncthreads();
-    const int per_row = D / 4;
-    const size_t stride = (size_t)kRowsPerWg * D;   // one split's partial O
-    for (int e = threadIdx.x; e < nrows * per_row; e += kAttnThreads) {
+    for (int e = threadIdx.x; e < n_el; e += kAttnThreads) {
         const int rr = e / per_row;
         const int d0 = (e % per_row) * 4;
-        const float* src = ws.part_o + ((size_t)slot0 * kRowsPerWg + rbase + rr) * D + d0;
+        const float* src = src_of(e);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        auto add = [&](float w, const float4& v) {
-            acc.x += w * v.x;
-            acc.y += w * v.y;
-            acc.z += w * v.z;
-            acc.w += w * v.w;
+        auto add = [&](float w, const f32x4& v) {
+            acc.x += w * v[0];
+            acc.y += w * v[1];
+            acc.z += w * v[2];
+            acc.w += w * v[3];
         };
         // the splits' loads are issued eight at a time before any of them
         // is used, so a unit of a few pieces waits for one round trip
-        constexpr int kInFlight = 8;
         for (int k0 = 0; k0 < ns; k0 += kInFlight) {
-            float4 v[kInFlight];
+            f32x4 v[kInFlight];
+            if (k0 == 0 && e == (int)threadIdx.x) {
 #pragma unroll
-            for (int j = 0; j < kInFlight; ++j)
-                if (k0 + j < ns)
-                    v[j] = *reinterpret_cast<const float4*>(src + (size_t)(k0 + j) * stride);
+                for (int j = 0; j < kInFlight; ++j) v[j] = first[j];
+            } else {
+#pragma unroll
+                for (int j = 0; j < kInFlight; ++j)
+                    v[j] = *reinterpret_cast<const f32x4*>(
+                        src + (size_t)min(k0 + j, ns - 1) * stride);
+            }
 #pragma unroll
             for (int j = 0; j < kInFlight; ++j)
                 if (k0 + j < ns) add(wgt[k0 + j][rr], v[j]);
@@ -1156,7 +1182,7 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
     z.off_items = take((size_t)z.item_cap * kIItemInts * sizeof(int32_t));
     z.off_units = take((size_t)z.unit_cap * 2 * sizeof(int32_t));
     z.off_counts = take(4 * sizeof(int32_t));
-    z.off_split = take((size_t)z.split_cap * sizeof(int32_t));
+    z.off_split = take((size_t)z.split_cap * sizeof(int4));
     if (sh->dtype == FB_BF16) {
         z.off_part_o = take((size_t)z.slot_cap * kRowsPerWg * D * sizeof(float));
         z.off_part_lse = take((size_t)z.slot_cap * kRowsPerWg * sizeof(float));
@@ -1191,7 +1217,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     AttnWs ws{reinterpret_cast<int32_t*>(base + z.off_items),
               reinterpret_cast<int32_t*>(base + z.off_units),
               reinterpret_cast<int32_t*>(base + z.off_counts),
-              reinterpret_cast<int32_t*>(base + z.off_split),
+              reinterpret_cast<int4*>(base + z.off_split),
               reinterpret_cast<float*>(base + z.off_part_o),
               reinterpret_cast<float*>(base + z.off_part_lse)};
     const int fixed_chunk = sh->kv_split > 0 ? sh->kv_split / kKeyTile : 0;
