@@ -104,9 +104,9 @@ hipError_t launch_window_prologue(const void* q_in, void* q_out, const void* k_n
 struct LmSizes {
     int n_rtiles;        // 256-token tiles over row_cap
     int n_vtiles;        // 256-id vocabulary tiles
-    int tiles_per_part;  // vocabulary tiles per partition
-    int P;               // partitions (partials per row)
-    size_t total;        // workspace bytes (row_cap * P partials)
+    int cu;              // compute units the partition count is chosen for
+    int grid;            // workgroups: the most any row count needs
+    size_t total;        // workspace bytes (256 partials per workgroup)
 };
 LmSizes lm_sizes(const fb_pack* pack, int V, int D, int cu_count);
 hipError_t launch_lmhead(const void* hidden, const void* weight, int D, int V,

@@ -18,6 +18,11 @@
 // lm_merge_kernel one wave per row: merges the row's partition partials in a
 //                 fixed order into the first partial of the update workspace
 //                 (the rest are set empty), the input of the update kernel.
+#include <climits>
+#include <map>
+#include <mutex>
+#include <tuple>
+
 #include "internal.h"
 #include "top.h"
 
@@ -37,23 +42,77 @@ constexpr int kStageBytes = 2 * kHalfBytes;       // W part, then H part
 constexpr int kStages = 2;
 constexpr int kMergeThreads = 256;
 
-__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// LDS reads drained, then a workgroup barrier.  The wait is the builtin, not
+// inline asm, so the compiler knows the reads issued before it are complete
+// and does not wait for them again after the barrier (behind newer reads).
+__device__ inline void lds_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt not waited
+    asm volatile("s_barrier" ::: "memory");
+}
 __device__ inline void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Vocabulary partitions for n_lt token tiles.  One workgroup runs per CU at
+// a time, so the kernel takes about (rounds of workgroups over the CUs) x
+// (tiles of the largest partition + a workgroup's fixed start and end,
+// about 1/8 of a tile); the partition count P minimizes that (the smallest
+// such P), with P <= kMaxParts.  Host and device evaluate the same integer
+// expression, so both sides agree on P.
+constexpr int kMaxParts = 1024;
+__host__ __device__ inline long long lm_cost(int n_lt, int nv, int cu, int P) {
+    return (long long)((n_lt * P + cu - 1) / cu) * (((nv + P - 1) / P) * 8 + 1);
+}
+inline int lm_parts_host(int n_lt, int nv, int cu) {
+    const int pmax = nv < kMaxParts ? nv : kMaxParts;
+    int best = 1;
+    long long best_c = lm_cost(n_lt, nv, cu, 1);
+    for (int P = 2; P <= pmax; ++P) {
+        const long long c = lm_cost(n_lt, nv, cu, P);
+        if (c < best_c) best_c = c, best = P;
+    }
+    return best;
+}
+// the same choice by one wave (lane i tries P = i + 1, i + 65, ...); every
+// lane returns it
+__device__ inline int lm_parts_dev(int n_lt, int nv, int cu) {
+    const int lane = threadIdx.x & 63;
+    const int pmax = nv < kMaxParts ? nv : kMaxParts;
+    long long key = LLONG_MAX;   // cost * 2048 + P: the minimum is the smallest P of least cost
+    for (int P = lane + 1; P <= pmax; P += 64) {
+        const long long k = lm_cost(n_lt, nv, cu, P) * 2048 + P;
+        key = k < key ? k : key;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const long long o = __shfl_xor(key, off, 64);
+        key = o < key ? o : key;
+    }
+    return __builtin_amdgcn_readfirstlane((int)(key & 2047));   // uniform: keeps it scalar
+}
 
 __global__ void __launch_bounds__(kLmThreads, 1)
 lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int D, int V,
-              int row_cap, int n_rtiles, int n_vtiles, int tiles_per_part, int P,
-              PackView pv, float4* __restrict__ part) {
+              int row_cap, int padded, int n_vtiles, int cu, PackView pv,
+              float4* __restrict__ part) {
     __shared__ __attribute__((aligned(16))) unsigned char lds[kStages * kStageBytes];
     __shared__ Top s_top[kTileT];
     __shared__ int s_live;
 
     const int tid = threadIdx.x;
-    const int rt = blockIdx.x % n_rtiles;
-    const int pidx = blockIdx.x / n_rtiles;
+    // token tiles that can hold live rows (ragged rows are the first
+    // header-count rows; padded rows sit anywhere below row_cap), and the
+    // partitions for them; block b is token tile b mod n_lt of partition
+    // b / n_lt (the grid covers the largest n_lt * P any row count can ask for)
+    const int n_lt = ((padded ? row_cap : pv.hdr[kHdrRows]) + kTileT - 1) / kTileT;
+    const int P = n_lt > 0 ? lm_parts_dev(n_lt, n_vtiles, cu) : 0;
+    if ((int)blockIdx.x >= n_lt * P) return;
+    const int rt = blockIdx.x % n_lt;
+    const int pidx = blockIdx.x / n_lt;
     const int row0 = rt * kTileT;
-    const int vt0 = pidx * tiles_per_part;
-    const int vt1 = min(n_vtiles, vt0 + tiles_per_part);
+    // partitions of floor or ceil(n_vtiles / P) tiles
+    const int vt0 = (int)((long long)pidx * n_vtiles / P);
+    const int vt1 = (int)((long long)(pidx + 1) * n_vtiles / P);
     if (vt0 >= vt1) return;
     // skip token tiles without a live row
     if (tid == 0) s_live = 0;
@@ -132,35 +191,27 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
         for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
     Top top[2] = {top_empty(), top_empty()};
 
-    // The six fragments of k step kk + 1 are read while the eight MFMAs of k
-    // step kk issue, so an MFMA never waits on the read right before it.
-    auto compute = [&](int stage) {
+    // Operand fragments of one k step (16 of K): four of W, two of H, in two
+    // register sets so the reads of k step kk + 1 overlap the eight MFMAs of
+    // k step kk.
+    constexpr int KK = kBK / 16;
+    bf16x8 a[2][4], b[2][2];
+    auto read = [&](int stage, int kk, int buf) {
         const unsigned char* st = lds + stage * kStageBytes;
-        constexpr int KK = kBK / 16;
-        bf16x8 a[2][4], b[2][2];
-        auto read = [&](int kk, int buf) {
-            const uint32_t ko = swz ^ (uint32_t)(kk << 5);
+        const uint32_t ko = swz ^ (uint32_t)(kk << 5);
 #pragma unroll
-            for (int vi = 0; vi < 4; ++vi)
-                a[buf][vi] = *reinterpret_cast<const bf16x8*>(st + a_row + vi * 32 * kRowBytes + ko);
+        for (int vi = 0; vi < 4; ++vi)
+            a[buf][vi] = *reinterpret_cast<const bf16x8*>(st + a_row + vi * 32 * kRowBytes + ko);
 #pragma unroll
-            for (int ti = 0; ti < 2; ++ti)
-                b[buf][ti] = *reinterpret_cast<const bf16x8*>(st + b_row + ti * 32 * kRowBytes + ko);
-        };
-        read(0, 0);
+        for (int ti = 0; ti < 2; ++ti)
+            b[buf][ti] = *reinterpret_cast<const bf16x8*>(st + b_row + ti * 32 * kRowBytes + ko);
+    };
+    // MFMAs x0 .. x1-1 of a k step (x = 2 vi + ti)
+    auto mfmas = [&](int buf, int x0 = 0, int x1 = 8) {
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            const int cur = kk & 1;
-            if (kk + 1 < KK) read(kk + 1, cur ^ 1);
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int vi = 0; vi < 4; ++vi)
-#pragma unroll
-                for (int ti = 0; ti < 2; ++ti)
-                    acc[vi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][vi], b[cur][ti],
-                                                                          acc[vi][ti], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-        }
+        for (int x = x0; x < x1; ++x)
+            acc[x >> 1][x & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                a[buf][x >> 1], b[buf][x & 1], acc[x >> 1][x & 1], 0, 0, 0);
     };
 
     // fold the finished tile vt into the running tops; lane value (vi, r)
@@ -209,35 +260,69 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
             for (int ti = 0; ti < 2; ++ti) acc[vi][ti] = floatx16{};
     };
 
-    // ---- main loop: double-buffered stages; the loads run one K step
-    // ahead, across tile boundaries
+    // ---- main loop over the partition's stages k (vocabulary tile
+    // vt0 + k / KS, K step k % KS) in two LDS slots; stage k + 1 is loaded
+    // while stage k is computed.  The last k step's fragments of a stage are
+    // read before the barrier that hands its slot back to the loader, and
+    // their MFMAs issue right after it, so the next stage's first reads
+    // overlap eight MFMAs instead of stalling the matrix core.
+    const int T = (vt1 - vt0) * KS;
+    int ld_vt = vt0, ld_ks = 0;      // next stage to load
     set_vtile(vt0);
-    issue(0, 0);
-    int nvt = vt0, nks = 1;        // next K step to load
-    if (nks == KS) {
-        nvt += 1;
-        nks = 0;
-        if (nvt < vt1) set_vtile(nvt);
-    }
-    int stage = 0;
-    for (int vt = vt0; vt < vt1; ++vt) {
-        for (int ks = 0; ks < KS; ++ks) {
-            wait_vm0();
-            lds_barrier();         // this step's stage landed; the other is free
-            if (nvt < vt1) {
-                issue(nks, stage ^ 1);
-                if (++nks == KS) {
-                    nks = 0;
-                    if (++nvt < vt1) set_vtile(nvt);
-                }
-            }
-            compute(stage);
-            stage ^= 1;
+    auto issue_next = [&](int k) {
+        issue(ld_ks, k & 1);
+        if (++ld_ks == KS) {
+            ld_ks = 0;
+            if (++ld_vt < vt1) set_vtile(ld_vt);
         }
+    };
+    issue_next(0);
+    wait_vm0();
+    lds_barrier();
+    if (T > 1) issue_next(1);
+    read(0, 0, 0);
+    // k steps 0 .. KK-2 of stage k: reads of step kk + 1 under the MFMAs of kk
+    auto body = [&](int slot) {
+#pragma unroll
+        for (int kk = 0; kk + 1 < KK; ++kk) {
+            read(slot, kk + 1, (kk + 1) & 1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(kk & 1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    int k = 0;
+    for (int vt = vt0; vt < vt1; ++vt) {
+        for (int ks = 0; ks + 1 < KS; ++ks, ++k) {
+            const int slot = k & 1;
+            body(slot);
+            wait_vm0();
+            lds_barrier();         // stage k + 1 landed; slot k & 1 is free
+            read(slot ^ 1, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas((KK - 1) & 1, 0, 2);
+            __builtin_amdgcn_sched_barrier(0);
+            if (k + 2 < T) issue_next(k + 2);   // under the MFMAs in flight
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas((KK - 1) & 1, 2, 8);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // the tile's last stage: its last MFMAs, then the fold (no fragments
+        // live across it), then the hand-over to the next stage
+        const int slot = k & 1;
+        body(slot);
+        mfmas((KK - 1) & 1);
         if ((vt + 1) * kTileV > V)
             fold(vt, std::true_type{});
         else
             fold(vt, std::false_type{});
+        if (k + 1 < T) {
+            wait_vm0();
+            lds_barrier();
+            if (k + 2 < T) issue_next(k + 2);
+            read(slot ^ 1, 0, 0);
+        }
+        ++k;
     }
 
     // ---- merge: lane halves, then the two vocabulary halves of each token
@@ -263,21 +348,26 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
             const int row = row0 + tok;
             const Top t = top_merge(top[ti], s_top[tok]);
             if (row < row_cap && pv.row_req[row] >= 0)
-                part[(size_t)row * P + pidx] = top_pack(t);
+                part[(size_t)blockIdx.x * kTileT + tok] = top_pack(t);
         }
     }
 }
 
-// One wave per row: partials k = lane, lane + 64, ... merged per lane in
+// One wave per row: partials k = lane, lane + 64, ... (partition k of the
+// row's token tile, written by block k * n_lt + tile) merged per lane in
 // increasing k, then across lanes by a fixed butterfly.
 __global__ void __launch_bounds__(kMergeThreads)
-lm_merge_kernel(const float4* __restrict__ lm_part, int P, PackView pv, int row_cap,
-                float4* __restrict__ upd_part, int nsplit) {
+lm_merge_kernel(const float4* __restrict__ lm_part, int n_vtiles, int cu, PackView pv,
+                int row_cap, int padded, float4* __restrict__ upd_part, int nsplit) {
     const int row = blockIdx.x * (kMergeThreads / 64) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= row_cap || pv.row_req[row] < 0) return;
+    const int n_lt = ((padded ? row_cap : pv.hdr[kHdrRows]) + kTileT - 1) / kTileT;
+    const int P = lm_parts_dev(n_lt, n_vtiles, cu);
+    const size_t base = (size_t)(row / kTileT) * kTileT + row % kTileT;
+    const size_t stride = (size_t)n_lt * kTileT;
     Top t = top_empty();
-    for (int k = lane; k < P; k += 64) t = top_merge(t, top_unpack(lm_part[(size_t)row * P + k]));
+    for (int k = lane; k < P; k += 64) t = top_merge(t, top_unpack(lm_part[base + k * stride]));
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         Top o;
@@ -297,14 +387,28 @@ LmSizes lm_sizes(const fb_pack* pack, int V, int D, int cu_count) {
     LmSizes z{};
     z.n_rtiles = (pack->row_cap + kTileT - 1) / kTileT;
     z.n_vtiles = (V + kTileV - 1) / kTileV;
-    // about 8 workgroups per compute unit over the token tiles' partitions
-    const int target = 8 * (cu_count > 0 ? cu_count : 256);
-    int P = (target + z.n_rtiles - 1) / z.n_rtiles;
-    if (P > z.n_vtiles) P = z.n_vtiles;
-    if (P < 1) P = 1;
-    z.tiles_per_part = (z.n_vtiles + P - 1) / P;
-    z.P = (z.n_vtiles + z.tiles_per_part - 1) / z.tiles_per_part;
-    z.total = (size_t)pack->row_cap * z.P * sizeof(float4);
+    z.cu = cu_count > 0 ? cu_count : 256;
+    // the grid: the largest n_lt * P over every count of token tiles the
+    // rows can fill (memoized: the search is over n_rtiles x kMaxParts)
+    static std::mutex mu;
+    static std::map<std::tuple<int, int, int>, int> memo;
+    const auto key = std::make_tuple(z.n_rtiles, z.n_vtiles, z.cu);
+    int grid = 0;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = memo.find(key);
+        if (it != memo.end()) {
+            grid = it->second;
+        } else {
+            for (int n = 1; n <= z.n_rtiles; ++n) {
+                const int g = n * lm_parts_host(n, z.n_vtiles, z.cu);
+                grid = g > grid ? g : grid;
+            }
+            memo.emplace(key, grid);
+        }
+    }
+    z.grid = grid;
+    z.total = (size_t)grid * kTileT * sizeof(float4);
     (void)D;
     return z;
 }
@@ -314,16 +418,17 @@ hipError_t launch_lmhead(const void* hidden, const void* weight, int D, int V,
                          const UpdateSizes& uz, hipStream_t stream) {
     PackView pv = pack_view(pack);
     float4* lm_part = static_cast<float4*>(lm_ws);
-    hipLaunchKernelGGL(lmhead_kernel, dim3((unsigned)(z.n_rtiles * z.P)), dim3(kLmThreads), 0,
-                       stream, static_cast<const uint16_t*>(hidden),
-                       static_cast<const uint16_t*>(weight), D, V, pack->row_cap, z.n_rtiles,
-                       z.n_vtiles, z.tiles_per_part, z.P, pv, lm_part);
+    hipLaunchKernelGGL(lmhead_kernel, dim3((unsigned)z.grid), dim3(kLmThreads), 0, stream,
+                       static_cast<const uint16_t*>(hidden), static_cast<const uint16_t*>(weight),
+                       D, V, pack->row_cap, pack->layout == FB_PADDED ? 1 : 0, z.n_vtiles, z.cu,
+                       pv, lm_part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int rows_per_wg = kMergeThreads / 64;
     hipLaunchKernelGGL(lm_merge_kernel,
                        dim3((unsigned)((pack->row_cap + rows_per_wg - 1) / rows_per_wg)),
-                       dim3(kMergeThreads), 0, stream, lm_part, z.P, pv, pack->row_cap,
+                       dim3(kMergeThreads), 0, stream, lm_part, z.n_vtiles, z.cu, pv,
+                       pack->row_cap, pack->layout == FB_PADDED ? 1 : 0,
                        static_cast<float4*>(upd_ws), uz.nsplit);
     return hipGetLastError();
 }
