@@ -230,16 +230,43 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
                     const int v = vbase + vi * 32 + (r >> 2) * 8 + (r & 3);
                     f[vi * 16 + r] = (!partial || v < V) ? acc[vi][ti][r] : -INFINITY;
                 }
-            float vmax = f[0];
+            // maxima of the four 16-id groups (one MFMA tile each), then the
+            // tile maximum
+            float g[4];
 #pragma unroll
-            for (int j = 1; j < 64; ++j) vmax = fmaxf(vmax, f[j]);
+            for (int vi = 0; vi < 4; ++vi) {
+                g[vi] = f[vi * 16];
+#pragma unroll
+                for (int r = 1; r < 16; ++r) g[vi] = fmaxf(g[vi], f[vi * 16 + r]);
+            }
+            const float vmax = fmaxf(fmaxf(g[0], g[1]), fmaxf(g[2], g[3]));
             Top& t = top[ti];
             if (vmax > t.m) {
 #pragma clang fp contract(off)
-                int j0 = 63;
+                // lowest position of the maximum: the first group that holds
+                // it (every earlier group is below it), then the first
+                // position inside that group
+                int gs = 3;
 #pragma unroll
-                for (int j = 63; j >= 0; --j)
-                    if (f[j] == vmax) j0 = j;
+                for (int vi = 2; vi >= 0; --vi)
+                    if (g[vi] == vmax) gs = vi;
+                // the group's values by bit masks (v_bfi: (m & a) | (~m & b)),
+                // so the selection stays free of branches
+                const uint32_t m1 = gs >= 1 ? ~0u : 0u, m2 = gs >= 2 ? ~0u : 0u,
+                               m3 = gs >= 3 ? ~0u : 0u;
+                auto bfi = [](uint32_t m, float a, float b) -> float {
+                    uint32_t r;
+                    asm("v_bfi_b32 %0, %1, %2, %3"
+                        : "=v"(r) : "v"(m), "v"(__float_as_uint(a)), "v"(__float_as_uint(b)));
+                    return __uint_as_float(r);
+                };
+                int r0 = 15;
+#pragma unroll
+                for (int r = 15; r >= 0; --r) {
+                    const float x = bfi(m3, f[48 + r], bfi(m2, f[32 + r], bfi(m1, f[16 + r], f[r])));
+                    if (x == vmax) r0 = r;
+                }
+                const int j0 = gs * 16 + r0;
                 const float nmL = scaled_ref(vmax);
                 t.s *= __builtin_amdgcn_exp2f(t.mL - nmL);
                 t.m = vmax;

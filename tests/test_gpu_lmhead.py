@@ -91,13 +91,19 @@ def test_lmhead_reduce_matches_oracle(name, V, D, sample):
     run_case(name, V, D, seed=3, sample=sample)
 
 
-def test_lmhead_exact_ties_take_the_lowest_id():
-    """Seven vocabulary rows of W made equal to 256 e_0 and every hidden state
-    given h_0 = 1: each row's logits then hold seven exact maxima of 256 (one
-    nonzero product, so no rounding on either side) at ids in both lane halves,
-    both waves of a tile, other tiles and the last partition.  The argmax is the
-    lowest of them, 13, on every row."""
-    tied = [13, 14, 17, 45, 141, 269]
+@pytest.mark.parametrize("tied", [
+    # lowest copy in the first 16-id group of its lane; copies in both lane
+    # halves, both waves of a tile, another tile and the last partition
+    [13, 14, 17, 45, 141, 269],
+    # lowest copy in the third group of its lane (ids 69 and 101 share a lane:
+    # groups 2 and 3), more in the other wave and the next tile
+    [69, 101, 229, 325],
+])
+def test_lmhead_exact_ties_take_the_lowest_id(tied):
+    """Vocabulary rows of W made equal to 256 e_0 and every hidden state given
+    h_0 = 1: each row's logits then hold exact maxima of 256 (one nonzero
+    product, so no rounding on either side) at the tied ids and the last id.
+    The argmax is the lowest of them on every row."""
 
     def edit(hid, weight):
         V = weight.shape[0]
@@ -109,9 +115,10 @@ def test_lmhead_exact_ties_take_the_lowest_id():
     wl, host, packed, g, rows, o, tie, tok0 = run_case(
         "hetero64", 157184, 256, seed=6, sample=96, edit=edit, B=16,
         prefix=("uniform", 64, 512))
-    assert np.all(o["xhat"] == 13) and np.all(o["gap"] == 0)
-    assert np.all(g["argmax"][rows] == 13)
-    assert np.all(o["Z"][:, 13] == 256.0)
+    lo = min(tied)
+    assert np.all(o["xhat"] == lo) and np.all(o["gap"] == 0)
+    assert np.all(g["argmax"][rows] == lo)
+    assert np.all(o["Z"][:, lo] == 256.0)
 
 
 def test_lmhead_reduce_then_update_matches_oracle_update():
