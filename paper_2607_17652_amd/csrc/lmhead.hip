@@ -103,23 +103,25 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
     // token tiles that can hold live rows (ragged rows are the first
     // header-count rows; padded rows sit anywhere below row_cap), and the
     // partitions for them; block b is token tile b mod n_lt of partition
-    // b / n_lt (the grid covers the largest n_lt * P any row count can ask for)
+    // b / n_lt, and workgroup i takes blocks i, i + gridDim.x, ...
     const int n_lt = ((padded ? row_cap : pv.hdr[kHdrRows]) + kTileT - 1) / kTileT;
     const int P = n_lt > 0 ? lm_parts_dev(n_lt, n_vtiles, cu) : 0;
-    if ((int)blockIdx.x >= n_lt * P) return;
-    const int rt = blockIdx.x % n_lt;
-    const int pidx = blockIdx.x / n_lt;
+    for (int blk = blockIdx.x; blk < n_lt * P; blk += gridDim.x) {
+    const int rt = blk % n_lt;
+    const int pidx = blk / n_lt;
     const int row0 = rt * kTileT;
     // partitions of floor or ceil(n_vtiles / P) tiles
     const int vt0 = (int)((long long)pidx * n_vtiles / P);
     const int vt1 = (int)((long long)(pidx + 1) * n_vtiles / P);
-    if (vt0 >= vt1) return;
-    // skip token tiles without a live row
+    if (vt0 >= vt1) continue;
+    // skip token tiles without a live row (the first barrier also keeps the
+    // previous block's last reads of s_live and s_top before these writes)
+    __syncthreads();
     if (tid == 0) s_live = 0;
     __syncthreads();
     if (tid < kTileT && row0 + tid < row_cap && pv.row_req[row0 + tid] >= 0) s_live = 1;
     __syncthreads();
-    if (!s_live) return;
+    if (!s_live) continue;
 
     const int wave = tid >> 6;
     const int lane = tid & 63;
@@ -375,8 +377,9 @@ lmhead_kernel(const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, in
             const int row = row0 + tok;
             const Top t = top_merge(top[ti], s_top[tok]);
             if (row < row_cap && pv.row_req[row] >= 0)
-                part[(size_t)blockIdx.x * kTileT + tok] = top_pack(t);
+                part[(size_t)blk * kTileT + tok] = top_pack(t);
         }
+    }
     }
 }
 
@@ -434,8 +437,11 @@ LmSizes lm_sizes(const fb_pack* pack, int V, int D, int cu_count) {
             memo.emplace(key, grid);
         }
     }
-    z.grid = grid;
+    // partials: one per block; workgroups: at most eight per CU, each taking
+    // blocks in turn (blocks past n_lt * P end at once, but each still holds
+    // its CU for a moment)
     z.total = (size_t)grid * kTileT * sizeof(float4);
+    z.grid = grid < 8 * z.cu ? grid : 8 * z.cu;
     (void)D;
     return z;
 }

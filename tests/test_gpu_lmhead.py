@@ -91,6 +91,14 @@ def test_lmhead_reduce_matches_oracle(name, V, D, sample):
     run_case(name, V, D, seed=3, sample=sample)
 
 
+def test_lmhead_workgroups_that_take_two_blocks():
+    """52 requests of four live blocks: 6656 rows = 26 token tiles, for which
+    the partition choice on a 256-CU device asks for 26 x 88 = 2288 blocks,
+    more than the 2048 workgroups launched, so 240 workgroups run a second
+    block (the grid-stride path)."""
+    run_case("long8", 157184, 512, seed=5, sample=64, B=52, prefix=("uniform", 64, 512))
+
+
 @pytest.mark.parametrize("tied", [
     # lowest copy in the first 16-id group of its lane; copies in both lane
     # halves, both waves of a tile, another tile and the last partition
