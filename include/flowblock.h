@@ -285,6 +285,28 @@ int fb_wavefront_attention(const void* q, const void* k_cache,
                            const fb_pack* pack, const fb_attn_shape* sh,
                            void* out, void* ws, size_t ws_bytes, void* stream);
 
+/* fb_wavefront_attention in two calls, so that its scheduling can overlap the
+ * window KV write (Sec. 4.1 / Eq. 5 as above).  fb_attention_plan writes the
+ * attention's work list for this pack into ws: it reads only the pack (the
+ * tiles of fb_pack_wavefronts), not q or the caches, so it may run on another
+ * stream while fb_write_window_kv runs.  fb_wavefront_attention_planned then
+ * runs the attention on that list, with the same arguments, results and
+ * errors as fb_wavefront_attention.  The caller orders the two (planned after
+ * plan, e.g. with an event) and keeps ws untouched between them; the pack
+ * must not change in between.  For FB_F32 the plan is empty and the planned
+ * call is the whole attention.
+ *   ws  device workspace of fb_attention_workspace_bytes bytes (the same
+ *       buffer in both calls)
+ * Errors as fb_wavefront_attention (the plan checks the pack, shape and
+ * workspace only). */
+int fb_attention_plan(const fb_pack* pack, const fb_attn_shape* sh, void* ws,
+                      size_t ws_bytes, void* stream);
+int fb_wavefront_attention_planned(const void* q, const void* k_cache,
+                                   const void* v_cache, const int32_t* page_table,
+                                   const fb_pack* pack, const fb_attn_shape* sh,
+                                   void* out, void* ws, size_t ws_bytes,
+                                   void* stream);
+
 /* ---- Eq. 1-3, Sec. 3.1, Alg. 1: denoise update -------------------------- */
 
 /* Workspace bytes for fb_denoise_update with this pack and vocabulary. */

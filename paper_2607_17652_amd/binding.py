@@ -39,7 +39,8 @@ EXPORTS = [
     "fb_version", "fb_last_error", "fb_pack_bytes", "fb_pack_get_offsets",
     "fb_pack_init", "fb_pack_wavefronts", "fb_pack_read_status",
     "fb_write_window_kv", "fb_attention_workspace_bytes",
-    "fb_wavefront_attention", "fb_update_workspace_bytes", "fb_denoise_update",
+    "fb_wavefront_attention", "fb_attention_plan", "fb_wavefront_attention_planned",
+    "fb_update_workspace_bytes", "fb_denoise_update",
     "fb_vocab_reduce", "fb_denoise_apply",
     "fb_synth_embed", "fb_synth_logits", "fb_decode_loop",
     "fb_lmhead_workspace_bytes", "fb_lmhead_reduce", "fb_window_prologue",
@@ -140,6 +141,9 @@ def lib():
             "fb_attention_workspace_bytes": (sz, [P(fb_pack), P(fb_attn_shape)]),
             "fb_wavefront_attention": (i32, [vp, vp, vp, vp, P(fb_pack),
                                              P(fb_attn_shape), vp, vp, sz, vp]),
+            "fb_attention_plan": (i32, [P(fb_pack), P(fb_attn_shape), vp, sz, vp]),
+            "fb_wavefront_attention_planned": (i32, [vp, vp, vp, vp, P(fb_pack),
+                                                     P(fb_attn_shape), vp, vp, sz, vp]),
             "fb_update_workspace_bytes": (sz, [P(fb_pack), i32]),
             "fb_denoise_update": (i32, [vp, i32, i32, vp, i32, vp, vp, vp, vp, vp,
                                         i32, P(fb_pack), P(fb_update_params), vp,
@@ -313,6 +317,21 @@ def fb_wavefront_attention(q, k_cache, v_cache, page_table, pack, shape, out,
                                         _ptr(page_table), pack.ref(),
                                         ctypes.byref(shape), _ptr(out), _ptr(ws),
                                         nbytes, _stream(stream)))
+
+
+def fb_attention_plan(pack, shape, ws, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().fb_attention_plan(pack.ref(), ctypes.byref(shape), _ptr(ws), nbytes,
+                                   _stream(stream)))
+
+
+def fb_wavefront_attention_planned(q, k_cache, v_cache, page_table, pack, shape, out,
+                                   ws, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().fb_wavefront_attention_planned(_ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                _ptr(page_table), pack.ref(),
+                                                ctypes.byref(shape), _ptr(out), _ptr(ws),
+                                                nbytes, _stream(stream)))
 
 
 # ------------------------------------------------------------------- update

@@ -219,10 +219,20 @@ size_t fb_attention_workspace_bytes(const fb_pack* pack, const fb_attn_shape* sh
     return fb::attention_sizes(pack, sh, cu_count()).total;
 }
 
-int fb_wavefront_attention(const void* q, const void* k_cache, const void* v_cache,
-                           const int32_t* page_table, const fb_pack* pack,
-                           const fb_attn_shape* sh, void* out, void* ws, size_t ws_bytes,
-                           void* stream) {
+namespace {
+
+static int check_attention_ws(const fb::AttnPlanSizes& z, const void* ws, size_t ws_bytes) {
+    if (ws_bytes < z.total || (z.total > 0 && !ws))
+        return fail(FB_E_WORKSPACE, "attention workspace has %zu bytes, needs %zu", ws_bytes,
+                    z.total);
+    if (ws && !aligned16(ws)) return fail(FB_E_INVAL, "workspace must be 16-byte aligned");
+    return FB_OK;
+}
+
+static int wavefront_attention(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* page_table, const fb_pack* pack,
+                        const fb_attn_shape* sh, void* out, void* ws, size_t ws_bytes,
+                        void* stream, bool planned) {
     int rc = check_pack(pack);
     if (rc) return rc;
     rc = check_shape(pack, sh);
@@ -232,14 +242,44 @@ int fb_wavefront_attention(const void* q, const void* k_cache, const void* v_cac
     if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out))
         return fail(FB_E_INVAL, "q, caches and out must be 16-byte aligned");
     const fb::AttnPlanSizes z = fb::attention_sizes(pack, sh, cu_count());
-    if (ws_bytes < z.total || (z.total > 0 && !ws))
-        return fail(FB_E_WORKSPACE, "attention workspace has %zu bytes, needs %zu", ws_bytes,
-                    z.total);
-    if (ws && !aligned16(ws)) return fail(FB_E_INVAL, "workspace must be 16-byte aligned");
+    rc = check_attention_ws(z, ws, ws_bytes);
+    if (rc) return rc;
     hipError_t e = fb::launch_attention(q, k_cache, v_cache, page_table, pack, sh, out, ws, z,
-                                        (hipStream_t)stream);
+                                        (hipStream_t)stream, planned);
     if (e != hipSuccess) return hip_fail(e, "attention launch");
     return ok();
+}
+
+}  // namespace
+
+int fb_wavefront_attention(const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* page_table, const fb_pack* pack,
+                           const fb_attn_shape* sh, void* out, void* ws, size_t ws_bytes,
+                           void* stream) {
+    return wavefront_attention(q, k_cache, v_cache, page_table, pack, sh, out, ws, ws_bytes,
+                               stream, false);
+}
+
+int fb_attention_plan(const fb_pack* pack, const fb_attn_shape* sh, void* ws, size_t ws_bytes,
+                      void* stream) {
+    int rc = check_pack(pack);
+    if (rc) return rc;
+    rc = check_shape(pack, sh);
+    if (rc) return rc;
+    const fb::AttnPlanSizes z = fb::attention_sizes(pack, sh, cu_count());
+    rc = check_attention_ws(z, ws, ws_bytes);
+    if (rc) return rc;
+    hipError_t e = fb::launch_attention_plan(pack, sh, ws, z, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "attention plan launch");
+    return ok();
+}
+
+int fb_wavefront_attention_planned(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* page_table, const fb_pack* pack,
+                                   const fb_attn_shape* sh, void* out, void* ws,
+                                   size_t ws_bytes, void* stream) {
+    return wavefront_attention(q, k_cache, v_cache, page_table, pack, sh, out, ws, ws_bytes,
+                               stream, true);
 }
 
 size_t fb_update_workspace_bytes(const fb_pack* pack, int V) {
@@ -249,7 +289,7 @@ size_t fb_update_workspace_bytes(const fb_pack* pack, int V) {
 
 namespace {
 
-int check_update_args(const fb_pack* pack, int V, const void* tokens, const void* conf,
+static int check_update_args(const fb_pack* pack, int V, const void* tokens, const void* conf,
                       const void* argmax, const void* st, const void* pe, const void* fin,
                       const fb_update_params* prm, int T_max, int n_max) {
     if (!tokens || !conf || !argmax || !st || !pe || !fin || !prm)
@@ -269,7 +309,7 @@ int check_update_args(const fb_pack* pack, int V, const void* tokens, const void
     return FB_OK;
 }
 
-int check_reduce_args(const fb_pack* pack, const void* logits, int V, int dtype) {
+static int check_reduce_args(const fb_pack* pack, const void* logits, int V, int dtype) {
     if (!logits) return fail(FB_E_INVAL, "logits is NULL");
     if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
     if (dtype != FB_BF16 && dtype != FB_F32)
@@ -279,7 +319,7 @@ int check_reduce_args(const fb_pack* pack, const void* logits, int V, int dtype)
     return FB_OK;
 }
 
-int check_ws(const void* ws, size_t ws_bytes, size_t need) {
+static int check_ws(const void* ws, size_t ws_bytes, size_t need) {
     if (ws_bytes < need || !ws)
         return fail(FB_E_WORKSPACE, "update workspace has %zu bytes, needs %zu", ws_bytes,
                     need);
@@ -306,7 +346,7 @@ int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack, v
 
 namespace {
 
-int check_lmhead(const fb_pack* pack, int V, int D) {
+static int check_lmhead(const fb_pack* pack, int V, int D) {
     int rc = check_pack(pack);
     if (rc) return rc;
     if (V < 1) return fail(FB_E_INVAL, "V must be >= 1");
@@ -458,14 +498,14 @@ int fb_denoise_update_noalloc(const void* logits, int V, int dtype, int32_t* tok
 
 namespace {
 
-bool exact_in(float a, int dtype) {
+static bool exact_in(float a, int dtype) {
     if (dtype == FB_F32) return true;
     uint32_t u;
     memcpy(&u, &a, 4);
     return (u & 0xffffu) == 0;   // a bf16 value: the low half of the float is zero
 }
 
-int check_model(const fb_synth_model* m, int V, int dtype) {
+static int check_model(const fb_synth_model* m, int V, int dtype) {
     if (!m) return fail(FB_E_INVAL, "model is NULL");
     if (V < 2) return fail(FB_E_INVAL, "the synthetic model needs V >= 2");
     if (dtype != FB_BF16 && dtype != FB_F32)
@@ -480,7 +520,7 @@ int check_model(const fb_synth_model* m, int V, int dtype) {
     return FB_OK;
 }
 
-int check_embed_args(const fb_pack* pack, const fb_attn_shape* sh, const void* q,
+static int check_embed_args(const fb_pack* pack, const fb_attn_shape* sh, const void* q,
                      const void* k_new, const void* v_new) {
     int rc = check_pack(pack);
     if (rc) return rc;
@@ -490,7 +530,7 @@ int check_embed_args(const fb_pack* pack, const fb_attn_shape* sh, const void* q
     return FB_OK;
 }
 
-int check_logit_args(const fb_req_state* st, const int32_t* tokens, int T_max,
+static int check_logit_args(const fb_req_state* st, const int32_t* tokens, int T_max,
                      const fb_pack* pack, const fb_synth_model* m, int V, int dtype,
                      const int32_t* pred, const void* logits) {
     int rc = check_pack(pack);
@@ -505,7 +545,7 @@ int check_logit_args(const fb_req_state* st, const int32_t* tokens, int T_max,
 }
 
 // Enqueue one step of the loop (validated by the caller).
-hipError_t enqueue_step(const fb_loop_args* a, const fb::AttnPlanSizes* az,
+static hipError_t enqueue_step(const fb_loop_args* a, const fb::AttnPlanSizes* az,
                         const fb::UpdateSizes& uz, hipStream_t s) {
     hipError_t e = fb::launch_loop_count(a->st, a->pack->B, a->counters, a->forwards, 1, s);
     if (e != hipSuccess) return e;

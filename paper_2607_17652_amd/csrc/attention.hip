@@ -1193,11 +1193,36 @@ AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
     return z;
 }
 
+namespace {
+
+AttnWs ws_view(void* wsp, const AttnPlanSizes& z) {
+    char* base = static_cast<char*>(wsp);
+    return AttnWs{reinterpret_cast<int32_t*>(base + z.off_items),
+                  reinterpret_cast<int32_t*>(base + z.off_units),
+                  reinterpret_cast<int32_t*>(base + z.off_counts),
+                  reinterpret_cast<int4*>(base + z.off_split),
+                  reinterpret_cast<float*>(base + z.off_part_o),
+                  reinterpret_cast<float*>(base + z.off_part_lse)};
+}
+
+}  // namespace
+
+hipError_t launch_attention_plan(const fb_pack* pack, const fb_attn_shape* sh, void* wsp,
+                                 const AttnPlanSizes& z, hipStream_t stream) {
+    if (sh->dtype == FB_F32) return hipSuccess;   // the fp32 path has no plan
+    const int fixed_chunk = sh->kv_split > 0 ? sh->kv_split / kKeyTile : 0;
+    const long long max_keys = (long long)sh->max_pages * sh->page_size;
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pack_view(pack),
+                       ws_view(wsp, z), sh->Hkv, z.row_groups, z.item_cap, z.slot_cap,
+                       z.split_cap, z.target_items, fixed_chunk, max_keys);
+    return hipGetLastError();
+}
+
 hipError_t launch_attention(const void* q, const void* k_cache,
                             const void* v_cache, const int32_t* page_table,
                             const fb_pack* pack, const fb_attn_shape* sh,
                             void* out, void* wsp, const AttnPlanSizes& z,
-                            hipStream_t stream) {
+                            hipStream_t stream, bool planned) {
     PackView pv = pack_view(pack);
     const int g = sh->Hq / sh->Hkv;
     const float scale = sh->sm_scale > 0.f ? sh->sm_scale
@@ -1213,19 +1238,8 @@ hipError_t launch_attention(const void* q, const void* k_cache,
                            sh->num_pages, scale);
         return hipGetLastError();
     }
-    char* base = static_cast<char*>(wsp);
-    AttnWs ws{reinterpret_cast<int32_t*>(base + z.off_items),
-              reinterpret_cast<int32_t*>(base + z.off_units),
-              reinterpret_cast<int32_t*>(base + z.off_counts),
-              reinterpret_cast<int4*>(base + z.off_split),
-              reinterpret_cast<float*>(base + z.off_part_o),
-              reinterpret_cast<float*>(base + z.off_part_lse)};
-    const int fixed_chunk = sh->kv_split > 0 ? sh->kv_split / kKeyTile : 0;
-    const long long max_keys = (long long)sh->max_pages * sh->page_size;
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pv,
-                       ws, sh->Hkv, z.row_groups, z.item_cap, z.slot_cap, z.split_cap,
-                       z.target_items, fixed_chunk, max_keys);
-    hipError_t e = hipGetLastError();
+    const AttnWs ws = ws_view(wsp, z);
+    hipError_t e = planned ? hipSuccess : launch_attention_plan(pack, sh, wsp, z, stream);
     if (e != hipSuccess) return e;
     int shift = 0;
     while ((1 << shift) < sh->page_size) ++shift;

@@ -72,11 +72,15 @@ struct AttnPlanSizes {
 };
 AttnPlanSizes attention_sizes(const fb_pack* pack, const fb_attn_shape* sh,
                               int cu_count);
+// the plan kernel alone (no-op for fp32)
+hipError_t launch_attention_plan(const fb_pack* pack, const fb_attn_shape* sh, void* ws,
+                                 const AttnPlanSizes& sz, hipStream_t stream);
+// plan (unless `planned`: ws already holds this pack's plan), attention, combine
 hipError_t launch_attention(const void* q, const void* k_cache,
                             const void* v_cache, const int32_t* page_table,
                             const fb_pack* pack, const fb_attn_shape* sh,
                             void* out, void* ws, const AttnPlanSizes& sz,
-                            hipStream_t stream);
+                            hipStream_t stream, bool planned = false);
 
 struct UpdateSizes {
     int nsplit;      // vocabulary partitions per row in the first pass

@@ -41,6 +41,11 @@ def test_library_exports_every_declared_symbol(lib):
                          capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\b(fb_\w+)\b", out))
     assert set(declared_functions()) <= exported
+    # no other unmangled (C-linkage) function leaks out of the library: the
+    # internal helpers of the C-ABI file are static
+    plain = {ln.split()[-1] for ln in out.splitlines()
+             if len(ln.split()) == 3 and ln.split()[1] in "TW" and not ln.split()[-1].startswith("_")}
+    assert plain == set(declared_functions()), sorted(plain ^ set(declared_functions()))
 
 
 def test_version_and_sizes(lib):
@@ -116,6 +121,23 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     rc = lib.fb_wavefront_attention(fake, fake, fake, fake, ctypes.byref(h),
                                     ctypes.byref(sh), fake, fake, 1 << 30, None)
     assert rc == fb.FB_E_INVAL
+    rc = lib.fb_wavefront_attention_planned(fake, fake, fake, fake, ctypes.byref(h),
+                                            ctypes.byref(sh), fake, fake, 1 << 30, None)
+    assert rc == fb.FB_E_INVAL
+    assert lib.fb_attention_plan(ctypes.byref(h), ctypes.byref(sh), fake, 1 << 30,
+                                 None) == fb.FB_E_INVAL
+    # the split calls check the workspace like the one-call form
+    sh = fb.make_shape(8, 4, 128, fb.FB_BF16, 32, 4, 8)
+    need = lib.fb_attention_workspace_bytes(ctypes.byref(h), ctypes.byref(sh))
+    assert need > 0
+    assert lib.fb_attention_plan(ctypes.byref(h), ctypes.byref(sh), fake, need - 1,
+                                 None) == fb.FB_E_WORKSPACE
+    assert lib.fb_wavefront_attention_planned(fake, fake, fake, fake, ctypes.byref(h),
+                                              ctypes.byref(sh), fake, fake, need - 1,
+                                              None) == fb.FB_E_WORKSPACE
+    assert lib.fb_wavefront_attention_planned(None, fake, fake, fake, ctypes.byref(h),
+                                              ctypes.byref(sh), fake, fake, need,
+                                              None) == fb.FB_E_INVAL
     sh = fb.make_shape(8, 4, 96, fb.FB_BF16, 32, 4, 8)          # head_dim 96
     rc = lib.fb_write_window_kv(fake, fake, fake, fake, fake, ctypes.byref(h),
                                 ctypes.byref(sh), None)

@@ -126,6 +126,40 @@ def test_repeat_is_bit_identical():
     assert torch.equal(tok1, step.tokens)
 
 
+@pytest.mark.parametrize("name,seed", [("long8", 5), ("hetero64", 6), ("tiny", 7)])
+def test_plan_beside_the_kv_write_equals_the_one_call_attention(name, seed):
+    """fb_attention_plan on a second stream while fb_write_window_kv runs, then
+    fb_wavefront_attention_planned: the same output, bit for bit, as
+    fb_wavefront_attention after the KV write (long8 splits every unit, so the
+    combine runs on the plan's split list; tiny is the fp32 path, which has no
+    plan)."""
+    wl, host, t, step = setup(name, seed)
+    log(f"[parity] plan beside the KV write: {name} seed={seed}")
+    step.pack_step()
+    step.kv_step()
+    step.attention_step()
+    torch.cuda.synchronize()
+    ref = step.out.clone()
+    step.out.zero_()
+    step.attn_ws.fill_(0xA5)       # no plan left over from the one-call run
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    packed = torch.cuda.Event()
+    planned = torch.cuda.Event()
+    step.pack_step()
+    packed.record(main)
+    side.wait_event(packed)
+    fb.fb_attention_plan(step.pack, step.shape, step.attn_ws, side)
+    planned.record(side)
+    step.kv_step()
+    main.wait_event(planned)
+    fb.fb_wavefront_attention_planned(t["q"], t["k_cache"], t["v_cache"], step.page_table,
+                                      step.pack, step.shape, step.out, step.attn_ws)
+    torch.cuda.synchronize()
+    assert torch.equal(step.out, ref)
+    assert fb.fb_pack_read_status(step.pack)["code"] == 0
+
+
 def test_ragged_and_padded_agree_bitwise():
     """The same per-position inputs packed ragged and padded give bit-identical
     per-position outputs and identical request state."""
