@@ -90,13 +90,20 @@ struct VecTraits<float> {
     __device__ static inline float scalar(const float* p) { return *p; }
 };
 
+// A row's nsplit workgroups take its 16-byte-aligned body in pieces of
+// kBatch loads per thread (32 KB), in turn: workgroup k reads pieces k,
+// k + nsplit, ...  Neighbouring workgroups then read neighbouring memory,
+// which the HBM serves faster than the same bytes in one contiguous share
+// per workgroup.
+constexpr int kVocabBatch = 4;
+
 template <typename T>
 __global__ void __launch_bounds__(kVocabThreads)
-vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
+vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit,
                   PackView pv, float4* __restrict__ part, int bl, int padded) {
     using VT = VecTraits<T>;
     constexpr int N = VT::N;
-    constexpr int kBatch = 4;
+    constexpr int kBatch = kVocabBatch;
     const int slot = blockIdx.x / nsplit;
     const int k = blockIdx.x % nsplit;
     int row = slot;
@@ -109,25 +116,24 @@ vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
     } else if (pv.row_req[row] < 0) {   // ragged rows are tile-major: live ones first
         return;
     }
-    const int v0 = k * chunk;
-    const int v1 = min(V, v0 + chunk);
     const T* rp = logits + (size_t)row * V;
     const int tid = threadIdx.x;
 
-    // Body [a, e) is 16-byte aligned in memory; head [v0, a) and tail [e, v1)
-    // are taken one element at a time by the first threads.
-    const size_t abs0 = (size_t)row * V + v0;
-    int a = v0 + (int)((N - (abs0 % N)) % N);
-    if (a > v1) a = v1;
-    int e = a + ((v1 - a) / N) * N;
+    // Body [a, e) is 16-byte aligned in memory; head [0, a) and tail [e, V)
+    // are taken one element at a time by the first threads of workgroup 0.
+    const size_t abs0 = (size_t)row * V;
+    int a = (int)((N - (abs0 % N)) % N);
+    if (a > V) a = V;
+    const int e = a + ((V - a) / N) * N;
 
     Top t = top_empty();
-    if (tid < a - v0) {
-        float f[1] = {VT::scalar(rp + v0 + tid)};
-        top_fold<1>(t, f, v0 + tid);
+    if (k == 0 && tid < a) {
+        float f[1] = {VT::scalar(rp + tid)};
+        top_fold<1>(t, f, tid);
     }
     const int stride = kVocabThreads * N;
-    for (int base = a + tid * N; base < e; base += kBatch * stride) {
+    const int piece = kBatch * stride;
+    for (int base = a + k * piece + tid * N; base < e; base += nsplit * piece) {
         uint4 raw[kBatch];
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
@@ -144,7 +150,7 @@ vocab_pass_kernel(const T* __restrict__ logits, int V, int nsplit, int chunk,
             }
         }
     }
-    if (tid < v1 - e) {
+    if (k == 0 && tid < V - e) {
         float f[1] = {VT::scalar(rp + e + tid)};
         top_fold<1>(t, f, e + tid);
     }
@@ -519,16 +525,16 @@ sync_window_kernel(PackView pv, int B, fb_req_state* __restrict__ st,
 UpdateSizes update_sizes(const fb_pack* pack, int V, int cu_count) {
     UpdateSizes z{};
     const int target = 8 * (cu_count > 0 ? cu_count : 256);
-    const int min_chunk = 2048;
+    // workgroups per row: enough for about eight per CU, at least two (their
+    // interleaved pieces read faster than one workgroup's whole row), at
+    // most one per 32 KB piece of the row and 64
+    const int pieces = (V + kVocabBatch * kVocabThreads * 8 - 1) / (kVocabBatch * kVocabThreads * 8);
     int ns = (target + pack->row_cap - 1) / pack->row_cap;
-    const int max_ns = V / min_chunk > 1 ? V / min_chunk : 1;
-    if (ns > max_ns) ns = max_ns;
+    if (ns < 2) ns = 2;
+    if (ns > pieces) ns = pieces;
     if (ns > 64) ns = 64;
     if (ns < 1) ns = 1;
-    int chunk = (V + ns - 1) / ns;
-    chunk = (chunk + 7) / 8 * 8;
-    z.nsplit = (V + chunk - 1) / chunk;
-    z.chunk = chunk;
+    z.nsplit = ns;
     z.off_rho = (size_t)pack->row_cap * z.nsplit * sizeof(float4);
     z.total = z.off_rho + ((size_t)pack->B * sizeof(double) + 15) / 16 * 16;
     return z;
@@ -543,11 +549,11 @@ hipError_t launch_vocab_reduce(const void* logits, int V, int dtype,
     if (dtype == FB_BF16) {
         hipLaunchKernelGGL(vocab_pass_kernel<uint16_t>, grid, dim3(kVocabThreads), 0,
                            stream, static_cast<const uint16_t*>(logits), V, z.nsplit,
-                           z.chunk, pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
+                           pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
     } else {
         hipLaunchKernelGGL(vocab_pass_kernel<float>, grid, dim3(kVocabThreads), 0,
                            stream, static_cast<const float*>(logits), V, z.nsplit,
-                           z.chunk, pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
+                           pv, part, pack->bl, pack->layout == FB_PADDED ? 1 : 0);
     }
     return hipGetLastError();
 }

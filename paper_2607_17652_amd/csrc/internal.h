@@ -83,8 +83,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
                             hipStream_t stream, bool planned = false);
 
 struct UpdateSizes {
-    int nsplit;      // vocabulary partitions per row in the first pass
-    int chunk;       // elements per partition (multiple of 8)
+    int nsplit;      // workgroups (partials) per row in the first pass
     size_t off_rho;  // per-request readiness of the window's last block
     size_t total;    // workspace bytes
 };

@@ -359,12 +359,13 @@ def _plant_neg_inf(logits, V):
             logits[r, V // 3] = keep
 
 
-@pytest.mark.parametrize("V", [157184, 1001])
+@pytest.mark.parametrize("V", [157184, 1001, 40009])
 def test_neg_inf_logits(V):
     """-inf logits weigh exp(-inf) = 0 (Eq. 1's softmax): runs of them at the
-    start of a vocabulary partition, over whole partitions, inside every
-    16-byte group and at an unaligned row head give the oracle's argmax and
-    confidence, and the same update."""
+    start of a workgroup's pieces, over every piece of some workgroups,
+    inside every 16-byte group and at an unaligned row head give the oracle's
+    argmax and confidence, and the same update (V = 40009: odd rows of three
+    32 KB pieces, one per workgroup)."""
     wl, host, t, step = setup("single", seed=13, V=V)
     log(f"[parity] -inf logits V={V} rows={wl.row_cap}")
     _plant_neg_inf(t["logits"], V)
@@ -419,7 +420,7 @@ def _plant_ties(logits, V, seed):
     return lowest
 
 
-@pytest.mark.parametrize("V", [157184, 5003])
+@pytest.mark.parametrize("V", [157184, 5003, 40009])
 def test_argmax_ties_take_the_lowest_id(V):
     """Exact ties at the maximum of a row (Eq. 1 takes the argmax; the
     lowest id wins a tie) planted across the vocabulary partitions, inside
