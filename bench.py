@@ -220,13 +220,14 @@ def cold_steps(torch, one_step, step, K, nph, flush_bytes=1 << 30):
             "steps": K, "flush_bytes": flush_bytes}
 
 
-def hbm_probe(torch, fb, nbytes=2 << 30, reps=5):
+def hbm_probe(torch, fb, nbytes=2 << 30, reps=5, logits=None):
     """Measured device-memory ceilings beside the 8 TB/s vendor figure, from
     the library's probes: a read-only stream with the vocabulary pass's load
     form (bytes read per second) and a plain copy (bytes read + written per
     second), each the best of `reps` launches timed with HIP events on the
     launch stream.  The read probe's XOR result is checked against the
-    buffer's known contents."""
+    buffer's known contents.  With `logits` (the live rows, contiguous) the
+    read probe also streams exactly the bytes the vocabulary pass reads."""
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(0x5a)
     dst = torch.empty_like(src)
     out = torch.empty(fb.FB_PROBE_BLOCKS, dtype=torch.int32, device="cuda")
@@ -252,10 +253,16 @@ def hbm_probe(torch, fb, nbytes=2 << 30, reps=5):
         xr ^= v
     t_copy = best(lambda: fb.fb_hbm_copy_probe(src, dst))
     del src, dst
-    return {"read_GBps": nbytes / t_read / 1e9, "copy_GBps": 2 * nbytes / t_copy / 1e9,
-            "read_xor_ok": xr == 0, "bytes": nbytes,
-            "note": "library probes (fb_hbm_read_probe, fb_hbm_copy_probe), best of 5; "
-                    "copy counts bytes read + written"}
+    res = {"read_GBps": nbytes / t_read / 1e9, "copy_GBps": 2 * nbytes / t_copy / 1e9,
+           "read_xor_ok": xr == 0, "bytes": nbytes,
+           "note": "library probes (fb_hbm_read_probe, fb_hbm_copy_probe), best of 5; "
+                   "copy counts bytes read + written"}
+    if logits is not None:
+        lb = logits.numel() * logits.element_size()
+        t_log = best(lambda: fb.fb_hbm_read_probe(logits, out))
+        res["read_GBps_live_logits"] = lb / t_log / 1e9
+        res["live_logit_bytes"] = lb
+    return res
 
 
 def graph_replay(torch, fb, step, one_step, copies, K, W):
@@ -587,7 +594,14 @@ def main():
         "plan_overlap": overlap,
     }
     out.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
-    out["hbm_probe"] = hbm_probe(torch, fb)
+    live_logits = t["logits"][:n_live] if wl.layout == "ragged" else None
+    out["hbm_probe"] = hbm_probe(torch, fb, logits=live_logits)
+    if live_logits is not None:
+        # the vocabulary pass against the same probe over the same bytes
+        out["vocab_pct_of_read_probe"] = (100.0 * head["roofline"]["achieved"] * 1e9
+                                          / (out["hbm_probe"]["read_GBps_live_logits"] * 1e9)
+                                          if head["roofline"]["kernel"] == "vocab_pass_kernel"
+                                          else None)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(wl, host, t, args.cpu_budget_s, args.seed)
         cb["host_cpus"] = os.cpu_count()

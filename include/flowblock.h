@@ -422,16 +422,17 @@ int fb_denoise_update_noalloc(const void* logits, int V, int dtype, int32_t* tok
 #define FB_PROBE_BLOCKS 2048
 
 /* Read-only stream over `bytes` of device memory at `src` with the load form
- * of the vocabulary pass (16-byte nontemporal loads, four in flight per
- * thread, a contiguous share per workgroup): the measured read ceiling the
+ * of the vocabulary pass (16-byte nontemporal loads), in the fastest read
+ * pattern measured (the workgroups walk the buffer together in 32 KB blocks,
+ * eight loads in flight per thread): the measured read ceiling the
  * vocabulary reduction is set against.  out (device uint32[FB_PROBE_BLOCKS])
- * receives, per workgroup, the XOR of the 32-bit words of its share; the XOR
- * of all of them is the XOR of every word of the buffer.
+ * receives, per workgroup, the XOR of the 32-bit words it read; the XOR of
+ * all of them is the XOR of every word of the buffer.
  *   src     16-byte aligned; bytes a positive multiple of 16 */
 int fb_hbm_read_probe(const void* src, size_t bytes, uint32_t* out, void* stream);
 
-/* Device copy of `bytes` from src to dst (16-byte loads and stores, the same
- * shares): the measured read+write ceiling.  Both 16-byte aligned, not
+/* Device copy of `bytes` from src to dst (16-byte loads and stores, a
+ * contiguous share per workgroup): the measured read+write ceiling.  Both 16-byte aligned, not
  * overlapping; bytes a positive multiple of 16. */
 int fb_hbm_copy_probe(const void* src, void* dst, size_t bytes, void* stream);
 
