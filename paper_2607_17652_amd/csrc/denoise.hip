@@ -20,15 +20,26 @@ namespace {
 constexpr int kVocabThreads = 512;   // 8 waves per (row, partition): measured 1% faster than 4
 constexpr int kUpdThreads = 256;
 
+// Maximum of the values (logits hold no NaN, so the max needs no quieting
+// of its inputs: three-input v_max3 steps instead of fmaxf chains).
+template <int N>
+__device__ inline float max_of(const float (&f)[N]) {
+    if constexpr (N == 1) {
+        return f[0];
+    } else {
+        float m = f[0];
+        int j = 1;
+        for (; j + 1 < N; j += 2)
+            asm("v_max3_f32 %0, %1, %2, %3" : "=v"(m) : "v"(m), "v"(f[j]), "v"(f[j + 1]));
+        if (j < N) asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(m), "v"(f[j]));
+        return m;
+    }
+}
+
 // Fold n consecutive values starting at index v into t (values in index order).
 template <int N>
 __device__ inline void top_fold(Top& t, const float (&f)[N], int v) {
-    float vmax = f[0];
-#pragma unroll
-    for (int j = 1; j < N; ++j) vmax = fmaxf(vmax, f[j]);
-    // A group of -inf logits adds exp(-inf) = 0.  Skipping it also keeps an
-    // empty running value (mL = -inf) away from the -inf + inf below.
-    if (vmax == -INFINITY) return;
+    const float vmax = max_of(f);
     if (vmax > t.m) {
 #pragma clang fp contract(off)
         int j0 = N - 1;
@@ -41,9 +52,13 @@ __device__ inline void top_fold(Top& t, const float (&f)[N], int v) {
         t.mL = nmL;
         t.idx = v + j0;
     }
+    // While t is empty (mL = -inf, only before the first finite value) the
+    // reference is the lowest finite float instead, so -inf logits give
+    // exp2(-inf) = 0 rather than -inf + inf: no branch on all -inf groups.
+    const float ref = fmaxf(t.mL, -3.402823466e38f);
     float e[N];
 #pragma unroll
-    for (int j = 0; j < N; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(f[j], kLog2e, -t.mL));
+    for (int j = 0; j < N; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(f[j], kLog2e, -ref));
 #pragma unroll
     for (int w = 1; w < N; w <<= 1)
 #pragma unroll
