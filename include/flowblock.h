@@ -356,7 +356,8 @@ int fb_denoise_update(const void* logits, int V, int dtype, int32_t* tokens,
  *
  * fb_vocab_reduce: step 1's streaming part (Eq. 1 symbols x_hat and p): for
  * every live packed row, partial (max, lowest argmax, sum of exponentials)
- * over vocabulary partitions, written to `ws`.  Reads each live logit once. */
+ * over vocabulary shares (a row's workgroups take its 32 KB pieces in turn),
+ * written to `ws`.  Reads each live logit once. */
 int fb_vocab_reduce(const void* logits, int V, int dtype, const fb_pack* pack,
                     void* ws, size_t ws_bytes, void* stream);
 

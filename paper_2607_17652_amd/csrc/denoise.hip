@@ -2,13 +2,14 @@
 // readiness (Eq. 2), post-edit bookkeeping (Sec. 3.1), in-order retirement and
 // readiness-gated admission (Alg. 1, Eq. 3).
 //
-// vocab_pass_kernel   one workgroup per (live row, vocabulary partition):
-//                     streams the logits once in 16-byte loads and keeps, per
-//                     thread, (max, lowest index of the max, sum of
+// vocab_pass_kernel   a few workgroups per live row, each taking every
+//                     nsplit-th 32 KB piece of the row: streams the logits
+//                     once in 16-byte loads and keeps, per thread, (max,
+//                     lowest index of the max, sum of
 //                     exp2(z*log2e - round(max*log2e))); wavefront butterfly
-//                     then LDS merge; one 16-byte partial per partition.
+//                     then LDS merge; one 16-byte partial per workgroup.
 // request_kernel      one workgroup per request: merges a row's partials in
-//                     partition order, applies Eq. 1, counts each live block,
+//                     workgroup order, applies Eq. 1, counts each live block,
 //                     then retires and admits on one thread.
 // Every reduction has a fixed order, so results are bit-reproducible.
 #include "internal.h"
