@@ -68,6 +68,10 @@ extern "C" {
                              gen_start + n*bl > T_max                        */
 #define FB_DERR_PAGE   2  /* a KV position past max_pages*page_size or a
                              page id outside [0, num_pages)                  */
+#define FB_DERR_PLAN   3  /* fb_wavefront_attention_planned found a work
+                             record the plan of this pack cannot hold (the
+                             workspace had no plan); recorded for request 0,
+                             the record skipped                              */
 
 /* ---- element types and packing layouts --------------------------------- */
 #define FB_F32   0

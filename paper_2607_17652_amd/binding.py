@@ -23,6 +23,7 @@ FB_E_HIP = -4
 FB_DERR_NONE = 0
 FB_DERR_STATE = 1
 FB_DERR_PAGE = 2
+FB_DERR_PLAN = 3
 
 FB_F32 = 0
 FB_BF16 = 1

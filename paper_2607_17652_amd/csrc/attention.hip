@@ -62,6 +62,19 @@ struct AttnWs {
     float* part_lse;   // [slot_cap][128]
 };
 
+// Capacities a plan record must respect to belong to this pack and shape.
+// The attention and the combine check every record they read against them,
+// so a workspace used without its plan (fb_wavefront_attention_planned
+// before fb_attention_plan) is reported, never followed out of bounds.
+struct PlanBounds {
+    int n_req;          // requests of the pack
+    int row_cap;        // packed rows
+    int unit_cap;       // units
+    int slot_cap;       // split partial slots
+    long long max_keys; // keys the page table can address
+};
+
+
 // ---------------------------------------------------------------- plan ----
 constexpr int kPlanThreads = 256;   // 4 waves: shorter barrier and scan rounds than 16 (measured 2-4%)
 constexpr int kPlanWaves = kPlanThreads / 64;
@@ -473,7 +486,8 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                  const uint16_t* __restrict__ v_cache,
                  const int32_t* __restrict__ page_table, PackView pv, AttnWs ws,
                  uint16_t* __restrict__ out, int Hq, int Hkv, int g, int bl, int RG,
-                 int ps, int ps_shift, int max_pages, int num_pages, float scale_log2) {
+                 int ps, int ps_shift, int max_pages, int num_pages, float scale_log2,
+                 PlanBounds bounds) {
     using RG_ = Ring<D>;
     constexpr int NS = RG_::kStages;
     __shared__ __attribute__((aligned(16))) unsigned char ring[NS * RG_::kStageBytes];
@@ -493,6 +507,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // the count check, which would serialize the two round trips)
     asm volatile("" :: "s"(u), "s"(kb), "s"(ke), "s"(slot), "s"(b), "s"(row0), "s"(n_items));
     if (item >= n_items) return;
+    if ((unsigned)u >= (unsigned)bounds.unit_cap || kb < 0 || (kb & (kKeyTile - 1)) != 0 ||
+        ke <= kb || (long long)ke > bounds.max_keys || slot < -1 || slot >= bounds.slot_cap ||
+        (unsigned)b >= (unsigned)bounds.n_req || row0 < 0 || row0 > bounds.row_cap - bl) {
+        if (threadIdx.x == 0) record_error(pv.hdr, 0, FB_DERR_PLAN);
+        return;
+    }
     const int rg = u % RG;
     const int c = (u / RG) % Hkv;
     const int32_t* pt = page_table + (size_t)b * max_pages;
@@ -978,7 +998,7 @@ constexpr int kCombineParts = kRowsPerWg / kCombineRows;
 template <typename T>
 __global__ void __launch_bounds__(kAttnThreads)
 combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
-               int g, int bl, int RG, int D) {
+               int g, int bl, int RG, int D, PlanBounds bounds) {
     __shared__ float wgt[kMaxSplits][kCombineRows];
     __shared__ float inv_den[kCombineRows];
     const int su = blockIdx.x / kCombineParts;
@@ -991,6 +1011,11 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
     if (ns <= 1) return;
     const int slot0 = rec.z;
     const int row0 = rec.w;
+    if ((unsigned)u >= (unsigned)bounds.unit_cap || ns > kMaxSplits || slot0 < 0 ||
+        slot0 > bounds.slot_cap - ns || row0 < 0 || row0 > bounds.row_cap - bl) {
+        if (threadIdx.x == 0) record_error(pv.hdr, 0, FB_DERR_PLAN);
+        return;
+    }
     const int rg = u % RG;
     const int c = (u / RG) % Hkv;
     const int rbase = part * kCombineRows;
@@ -1239,6 +1264,8 @@ hipError_t launch_attention(const void* q, const void* k_cache,
         return hipGetLastError();
     }
     const AttnWs ws = ws_view(wsp, z);
+    const PlanBounds bounds{pack->B, pack->row_cap, z.unit_cap, z.slot_cap,
+                            (long long)sh->max_pages * sh->page_size};
     hipError_t e = planned ? hipSuccess : launch_attention_plan(pack, sh, wsp, z, stream);
     if (e != hipSuccess) return e;
     int shift = 0;
@@ -1252,7 +1279,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     auto launch = [&](auto kernel) {
         hipLaunchKernelGGL(kernel, dim3(z.item_cap), dim3(kAttnThreads), 0, stream, qb, kc, vc,
                            page_table, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl, z.row_groups,
-                           sh->page_size, shift, sh->max_pages, sh->num_pages, scale_log2);
+                           sh->page_size, shift, sh->max_pages, sh->num_pages, scale_log2, bounds);
     };
     switch (sh->head_dim) {
         case 32:
@@ -1272,7 +1299,7 @@ hipError_t launch_attention(const void* q, const void* k_cache,
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(combine_kernel<uint16_t>, dim3(z.split_cap * kCombineParts), dim3(kAttnThreads),
                        0, stream, pv, ws, ob, sh->Hq, sh->Hkv, g, pack->bl,
-                       z.row_groups, sh->head_dim);
+                       z.row_groups, sh->head_dim, bounds);
     return hipGetLastError();
 }
 

@@ -160,6 +160,34 @@ def test_plan_beside_the_kv_write_equals_the_one_call_attention(name, seed):
     assert fb.fb_pack_read_status(step.pack)["code"] == 0
 
 
+def test_planned_attention_without_a_plan_is_reported():
+    """fb_wavefront_attention_planned on a workspace that holds no plan (every
+    byte 0x7F: each count is a large positive number and every record field
+    lies outside the pack's capacities) reads no record outside its bounds:
+    every record is skipped, FB_DERR_PLAN is recorded, and a real plan
+    afterwards gives the one-call output again."""
+    wl, host, t, step = setup("long8", seed=8)
+    log("[parity] planned attention without a plan: long8 seed=8")
+    step.pack_step()
+    step.kv_step()
+    step.attention_step()
+    torch.cuda.synchronize()
+    ref = step.out.clone()
+    step.attn_ws.fill_(0x7F)
+    fb.fb_wavefront_attention_planned(t["q"], t["k_cache"], t["v_cache"], step.page_table,
+                                      step.pack, step.shape, step.out, step.attn_ws)
+    torch.cuda.synchronize()
+    s = fb.fb_pack_read_status(step.pack)
+    assert s["code"] == fb.FB_DERR_PLAN and s["request"] == 0
+    step.pack_step()                       # a fresh pack clears the status word
+    fb.fb_attention_plan(step.pack, step.shape, step.attn_ws)
+    fb.fb_wavefront_attention_planned(t["q"], t["k_cache"], t["v_cache"], step.page_table,
+                                      step.pack, step.shape, step.out, step.attn_ws)
+    torch.cuda.synchronize()
+    assert fb.fb_pack_read_status(step.pack)["code"] == fb.FB_DERR_NONE
+    assert torch.equal(step.out, ref)
+
+
 def test_ragged_and_padded_agree_bitwise():
     """The same per-position inputs packed ragged and padded give bit-identical
     per-position outputs and identical request state."""
