@@ -430,12 +430,12 @@ __device__ inline float wave_xor32_max(float x) {
 // are issued from inline asm so the compiler neither sees nor waits on them;
 // the kernel orders them itself with explicit vmcnt waits and raw barriers.
 template <int N, typename F, int... I>
-__device__ inline void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+__device__ __attribute__((always_inline)) inline void static_for_impl(F& f, std::integer_sequence<int, I...>) {
     (f(std::integral_constant<int, I>{}), ...);
 }
 // f(std::integral_constant<int, 0>) ... f(std::integral_constant<int, N-1>)
 template <int N, typename F>
-__device__ inline void static_for(F&& f) {
+__device__ __attribute__((always_inline)) inline void static_for(F&& f) {
     static_for_impl<N>(f, std::make_integer_sequence<int, N>{});
 }
 
@@ -495,6 +495,11 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     constexpr int DT = D / 32;      // 32-wide d tiles of O^T
     constexpr int NCH = RG_::kPerThread;
     constexpr int CPR = D / 8;      // 16-byte chunks per K row
+    // A thread's loads j < NK fetch K and the rest V^T, for every wave when
+    // the K chunks fill whole loads.  Then (D = 128) K and V^T are refilled
+    // separately, K one step ahead (the split ring below).
+    constexpr int NK = RG_::kKCh / kAttnThreads;
+    constexpr bool SPLIT_RING = NS == 3 && RG_::kKCh % kAttnThreads == 0;
 
     // The item's record is read together with the item count (the grid has
     // item_cap workgroups, so the record is always inside the buffer).
@@ -604,8 +609,12 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // is off the path.
     auto tile_page = [&](int kt) -> int { return pt[(kt * kKeyTile) >> ps_shift]; };
     bool page_err = false;   // a bad page id on the whole-tile path (recorded once at the end)
-    auto issue_tile = [&](int kt, auto stage_c, int page) {
+    // PART 0: the tile's K loads, 1: its V^T loads, 2: both
+    auto issue_part = [&](int kt, auto stage_c, int page, auto part_c) __attribute__((always_inline)) {
         constexpr int STAGE = decltype(stage_c)::value;
+        constexpr int PART = decltype(part_c)::value;
+        constexpr int J0 = PART == 1 ? NK : 0;
+        constexpr int J1 = PART == 0 ? NK : NCH;
         const int key0 = kt * kKeyTile;
         if (FAST) {
             // one page per tile: uniform base + per-lane constant offsets
@@ -617,7 +626,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             const unsigned char* kbase = kb0 + poff + inpage * (uint32_t)(D * 2);
             const unsigned char* vbase = vb0 + poff + inpage * 2u;
 #pragma unroll
-            for (int j = 0; j < NCH; ++j) {
+            for (int j = J0; j < J1; ++j) {
                 const uint32_t m0 = m0_base[j] + STAGE * RG_::kStageBytes;
                 // for D >= 64 the K chunks are exactly the first kKCh/256 loads
                 const bool isk = (RG_::kKCh % kAttnThreads == 0) ? (j * kAttnThreads < RG_::kKCh)
@@ -637,7 +646,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
             for (int i = 0; i < 4; ++i)
                 pid[i] = (i < npg && pbase + i <= plast) ? pt[pbase + i] : -1;
 #pragma unroll
-            for (int j = 0; j < NCH; ++j) {
+            for (int j = J0; j < J1; ++j) {
                 const int kg = key0 + ch_key[j];
                 const int pi = (kg >> ps_shift) - pbase;
                 int page = pid[0];
@@ -660,6 +669,9 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
                              :: "s"(m0), "v"(src) : "memory");
             }
         }
+    };
+    auto issue_tile = [&](int kt, auto stage_c, int page) {
+        issue_part(kt, stage_c, page, std::integral_constant<int, 2>{});
     };
 
     floatx16 o[DT];
@@ -825,7 +837,8 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
 
     // Software pipeline over key tiles, one step per tile i < nt-1:
     //   wait for tile i+1 and barrier; refill the stage of tile i-1 (read by
-    //   every wave before this barrier) with tile i+NS-1;
+    //   every wave before this barrier) with tile i+NS-1 (the split ring
+    //   refills the halves separately, see there);
     //   phase 1: S^T(i+1) on the matrix core while the VALU turns S^T(i)
     //            into P^T(i);
     //   phase 2: O^T += V^T(i) P^T(i) while the VALU takes the row max of
@@ -874,39 +887,138 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         s_cur = s_nxt;
     };
 
-    if (nt > 0) {
-        int pg0[NS - 1];   // page ids of the first tiles, all requested before any load
-        static_for<NS - 1>([&](auto j) { pg0[j] = (FAST && j < nt) ? tile_page(kt0 + j) : 0; });
-        static_for<NS - 1>([&](auto j) {
-            if (j < nt) issue_tile(kt0 + j, j, pg0[j]);
-        });
+    // The split ring (D = 128, three stages).  K(t) and V^T(t) still share
+    // stage t % 3, but the K half is free a step before the V^T half (the
+    // scores of tile t are taken in step t-1, its PV product in step t), so
+    // step i refills them separately: K(i+3) into the K half of tile i's
+    // stage and V^T(i+2) into the V^T half of tile i-1's.  Both then arrive
+    // two steps before use (one for K when a tile's halves move together),
+    // and step i waits only for what it reads -- K(i+1) and V^T(i), loaded
+    // in step i-2 -- while the loads of step i-1 stay in flight.
+    // KIND 0: both refills, no runtime checks; 1: a step near the end
+    // (K(i+3) may not exist); 2: step nt-2, which takes the last tile's
+    // scores and leaves only V^T(nt-1) in flight.
+    int pg_k = 0, pg_v = 0;   // page ids of the next K and V^T tiles to load
+    auto step_split = [&](int i, auto stage_c, auto kind_c) __attribute__((always_inline)) {
+        constexpr int STAGE = decltype(stage_c)::value;
+        constexpr int KIND = decltype(kind_c)::value;
+        constexpr int NXT = (STAGE + 1) % NS;
+        constexpr int FREE = (STAGE + NS - 1) % NS;
+        using KPart = std::integral_constant<int, 0>;
+        using VPart = std::integral_constant<int, 1>;
+        // step i-1 loaded K(i+2) (when i+2 < nt, true but in the last step)
+        // and V^T(i+1)
+        wait_vm(KIND == 2 ? NCH - NK : NCH);
+        barrier_raw();
+        if constexpr (KIND != 2) {
+            if (KIND == 0 || i + 3 < nt) issue_part(kt0 + i + 3, stage_c, pg_k, KPart{});
+            issue_part(kt0 + i + 2, std::integral_constant<int, FREE>{}, pg_v, VPart{});
+            if (FAST) {
+                pg_v = pg_k;
+                const int nx = i + 4 < nt ? i + 4 : nt - 1;   // clamped: no branch
+                pg_k = tile_page(kt0 + nx);
+            }
+        }
+        const unsigned char* kst = ring + NXT * RG_::kStageBytes;
+        const unsigned char* vst = ring + STAGE * RG_::kStageBytes;
+        floatx16 s_nxt = floatx16{};
+        phase1(kst, s_cur, s_nxt);
+        if constexpr (KIND == 2) {
+            if (valid_last < kKeyTile) mask_tail(s_nxt);
+        }
+        const float mx = phase2(vst, s_nxt);
+        update_max(mx);
+        s_cur = s_nxt;
+    };
+
+    if constexpr (SPLIT_RING) if (nt > 0) {
+        using C0 = std::integral_constant<int, 0>;
+        using C1 = std::integral_constant<int, 1>;
+        using C2 = std::integral_constant<int, 2>;
+        using KPart = std::integral_constant<int, 0>;
+        using VPart = std::integral_constant<int, 1>;
+        const int p0 = FAST ? tile_page(kt0) : 0;
+        const int p1 = (FAST && nt > 1) ? tile_page(kt0 + 1) : 0;
+        const int p2 = (FAST && nt > 2) ? tile_page(kt0 + 2) : 0;
+        // K(0), K(1), V^T(0), then Q; the first wait lets the later ring
+        // loads stay in flight (Q is waited for where it is used)
+        issue_part(kt0, C0{}, p0, KPart{});
+        if (nt > 1) issue_part(kt0 + 1, C1{}, p1, KPart{});
+        issue_part(kt0, C0{}, p0, VPart{});
         load_q();
-        wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
+        wait_vm(nt > 1 ? NCH : NCH - NK);
         barrier_raw();
         s_mfmas(ring, s_cur);
+        // the loads "step -1" makes: K(2) and V^T(1)
+        if (nt > 2) issue_part(kt0 + 2, C2{}, p2, KPart{});
+        if (nt > 1) issue_part(kt0 + 1, C1{}, p1, VPart{});
+        if (FAST) {
+            pg_v = p2;
+            pg_k = nt > 3 ? tile_page(kt0 + 3) : p2;
+        }
         if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
         m_run = tile_max(s_cur);
         thr_raw = (m_run + kRescaleSlack) / scale_log2;
         using Full = std::integral_constant<int, 0>;
         using Near = std::integral_constant<int, 1>;
         using Last = std::integral_constant<int, 2>;
-        // steps 0 .. n_full-1 refill the ring (and, as NS >= 3, are not the last)
-        const int n_full = nt - NS + 1 > 0 ? nt - NS + 1 : 0;
+        // steps 0 .. nt-4 make both refills; the tail steps check (one
+        // runtime-checked kind keeps the register pressure of the loop down)
+        const int n_full = nt - 3 > 0 ? nt - 3 : 0;
         int i0 = 0;
         for (; i0 + NS <= n_full; i0 += NS) {
-            static_for<NS>([&](auto j) { step(i0 + j, j, Full{}); });
+            static_for<NS>([&](auto j) { step_split(i0 + j, j, Full{}); });
         }
         for (; i0 < nt - 2; i0 += NS) {
             static_for<NS>([&](auto j) {
-                if (i0 + j < nt - 2) step(i0 + j, j, Near{});
+                if (i0 + j < nt - 2) step_split(i0 + j, j, Near{});
             });
         }
-        // the step that brings in the last tile (which may be partial)
         if (nt >= 2) {
-            const int st2 = (nt - 2) % NS;
+            const int st = (nt - 2) % NS;
             static_for<NS>([&](auto j) {
-                if (st2 == j) step(nt - 2, j, Last{});
+                if (st == j) step_split(nt - 2, j, Last{});
             });
+        }
+        // V^T of the last tile
+        wait_vm(0);
+        barrier_raw();
+    }
+    if (nt > 0) {
+        if constexpr (!SPLIT_RING) {
+            int pg0[NS - 1];   // page ids of the first tiles, all requested before any load
+            static_for<NS - 1>([&](auto j) { pg0[j] = (FAST && j < nt) ? tile_page(kt0 + j) : 0; });
+            static_for<NS - 1>([&](auto j) {
+                if (j < nt) issue_tile(kt0 + j, j, pg0[j]);
+            });
+            load_q();
+            wait_vm((nt - 1 < NS - 2 ? nt - 1 : NS - 2) * NCH);
+            barrier_raw();
+            s_mfmas(ring, s_cur);
+            if (nt == 1 && valid_last < kKeyTile) mask_tail(s_cur);
+            m_run = tile_max(s_cur);
+            thr_raw = (m_run + kRescaleSlack) / scale_log2;
+            using Full = std::integral_constant<int, 0>;
+            using Near = std::integral_constant<int, 1>;
+            using Last = std::integral_constant<int, 2>;
+            // steps 0 .. n_full-1 refill the ring (and, as NS >= 3, are not the last)
+            const int n_full = nt - NS + 1 > 0 ? nt - NS + 1 : 0;
+            int i0 = 0;
+            for (; i0 + NS <= n_full; i0 += NS) {
+                static_for<NS>([&](auto j) { step(i0 + j, j, Full{}); });
+            }
+            for (; i0 < nt - 2; i0 += NS) {
+                static_for<NS>([&](auto j) {
+                    if (i0 + j < nt - 2) step(i0 + j, j, Near{});
+                });
+            }
+            // the step that brings in the last tile (which may be partial)
+            if (nt >= 2) {
+                const int st2 = (nt - 2) % NS;
+                static_for<NS>([&](auto j) {
+                    if (st2 == j) step(nt - 2, j, Last{});
+                });
+            }
         }
         // last tile: P^T, then its PV product
         softmax_p(s_cur);

@@ -105,6 +105,18 @@ def test_fp32_bigger_shapes():
                     window=("uniform", 1, 3), V=5003, prefix_jitter=9)
 
 
+@pytest.mark.parametrize("kv_split,ps", [(32, 32), (64, 32), (96, 32), (128, 32), (160, 32),
+                                         (64, 16), (128, 16)])
+def test_short_items_take_every_ring_tail(kv_split, ps):
+    """A fixed split of kv_split keys makes items of one to five key tiles, so
+    the d = 128 ring runs every short schedule: a lone tile, a last step only,
+    near-end steps with and without a K refill, and a full step before them;
+    jittered prefixes leave the last tile partial, and pages of 16 keys take
+    the per-lane page path."""
+    run_and_compare("single", kv_split=kv_split, B=3, page_size=ps, V=5003,
+                    prefix=("uniform", 20, 400), window=("uniform", 1, 3), prefix_jitter=13)
+
+
 def test_explicit_kv_split_matches_oracle():
     run_and_compare("hetero64", reqs=list(range(0, 64, 7)), kv_split=256)
 
