@@ -42,6 +42,7 @@ constexpr int kWgsPerCu = 3;          // resident attention workgroups per CU
 constexpr int kKeyTile = 32;
 constexpr int kMinChunkTiles = 4;   // never split below 128 keys
 constexpr int kMaxSplits = 64;      // splits of one unit the combine can merge
+constexpr int kMaxHeadDim = 128;    // largest head_dim built (32, 64, 128)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;  // lazy rescale: running max may lag by 2^8
 
@@ -838,7 +839,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // Software pipeline over key tiles, one step per tile i < nt-1:
     //   wait for tile i+1 and barrier; refill the stage of tile i-1 (read by
     //   every wave before this barrier) with tile i+NS-1 (the split ring
-    //   refills the halves separately, see there);
+    //   below waits and refills per half instead);
     //   phase 1: S^T(i+1) on the matrix core while the VALU turns S^T(i)
     //            into P^T(i);
     //   phase 2: O^T += V^T(i) P^T(i) while the VALU takes the row max of
@@ -847,7 +848,7 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
     // Stages in use: i (V), i+1 (K), i+2 .. i+NS-1 in flight.
     static_assert(NS >= 3, "the ring needs the current, next and one loading stage");
     floatx16 s_cur = floatx16{};
-    int pg_next = (FAST && NS - 1 < nt) ? tile_page(kt0 + NS - 1) : 0;
+    int pg_next = (!SPLIT_RING && FAST && NS - 1 < nt) ? tile_page(kt0 + NS - 1) : 0;
     // KIND 0: a step with a refill and the steady-state wait (no runtime
     // checks); 1: a step near the end; 2: the step that brings in the last
     // tile (which may be partial).
@@ -1140,10 +1141,84 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
         return ws.part_o + ((size_t)slot0 * kRowsPerWg + rbase + e / per_row) * D +
                (e % per_row) * 4;
     };
-    // A thread's first column group: its splits' loads (up to eight) are
-    // issued before the weights below are ready, so they overlap.
-    constexpr int kInFlight = 8;
     typedef float f32x4 __attribute__((ext_vector_type(4)));
+    // A row's split weights exp2(lse_k - max) and 1/sum: its log-sum-exps
+    // are loaded eight at a time (one round trip for up to eight splits) and
+    // kept in LDS until the maximum is known.
+    auto weights = [&]() {
+        if (threadIdx.x < nrows) {
+            const float* lse = ws.part_lse + (size_t)slot0 * kRowsPerWg + rbase + threadIdx.x;
+            float mx = -INFINITY;
+            for (int k0 = 0; k0 < ns; k0 += 8) {
+                float l[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) l[j] = lse[(size_t)min(k0 + j, ns - 1) * kRowsPerWg];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) mx = fmaxf(mx, l[j]);   // repeats do not move it
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (k0 + j < ns) wgt[k0 + j][threadIdx.x] = l[j];
+            }
+            float den = 0.f;
+            for (int k = 0; k < ns; ++k) {
+                const float w = __builtin_amdgcn_exp2f(wgt[k][threadIdx.x] - mx);
+                wgt[k][threadIdx.x] = w;
+                den += w;
+            }
+            inv_den[threadIdx.x] = 1.0f / den;
+        }
+        __syncthreads();
+    };
+    auto store = [&](int e, const float4& acc) {
+        const int rr = e / per_row;
+        const int d0 = (e % per_row) * 4;
+        const float id = inv_den[rr];
+        const int r = rg * kRowsPerWg + rbase + rr;
+        const int pos_local = r / g, hg = r % g;
+        T* dst = out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d0;
+        store_out4<T>(dst, make_float4(acc.x * id, acc.y * id, acc.z * id, acc.w * id));
+    };
+    auto add = [](float4& acc, float w, const f32x4& v) {
+        acc.x += w * v[0];
+        acc.y += w * v[1];
+        acc.z += w * v[2];
+        acc.w += w * v[3];
+    };
+    // Up to kFastSplits splits (the plan's usual few pieces): every load of
+    // the thread's column groups (at most kMaxGroups) is issued before the
+    // weights are computed, so the workgroup waits for one round trip.
+    constexpr int kFastSplits = 4;
+    constexpr int kMaxGroups = kCombineRows * kMaxHeadDim / 4 / kAttnThreads;
+    const int n_grp = (n_el + kAttnThreads - 1) / kAttnThreads;   // workgroup-uniform
+    if (ns <= kFastSplits && n_grp <= kMaxGroups) {
+        f32x4 v[kMaxGroups][kFastSplits];
+#pragma unroll
+        for (int m = 0; m < kMaxGroups; ++m) {
+            if (m < n_grp) {
+                const float* src = src_of(min((int)threadIdx.x + m * kAttnThreads, n_el - 1));
+#pragma unroll
+                for (int k = 0; k < kFastSplits; ++k)   // past the last split: reload it, unused
+                    v[m][k] = *reinterpret_cast<const f32x4*>(src + (size_t)min(k, ns - 1) * stride);
+            }
+        }
+        weights();
+#pragma unroll
+        for (int m = 0; m < kMaxGroups; ++m) {
+            const int e = (int)threadIdx.x + m * kAttnThreads;
+            if (m < n_grp && e < n_el) {
+                const int rr = e / per_row;
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int k = 0; k < kFastSplits; ++k)
+                    if (k < ns) add(acc, wgt[k][rr], v[m][k]);
+                store(e, acc);
+            }
+        }
+        return;
+    }
+    // More splits: a thread's first column group has its loads (up to eight)
+    // issued before the weights are ready; then eight at a time per group.
+    constexpr int kInFlight = 8;
     f32x4 first[kInFlight];
     {
         const float* src = src_of(min((int)threadIdx.x, n_el - 1));
@@ -1153,32 +1228,11 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
 #pragma unroll
         for (int j = 0; j < kInFlight; ++j) asm volatile("" :: "v"(first[j]));
     }
-    if (threadIdx.x < nrows) {
-        const float* lse = ws.part_lse + (size_t)slot0 * kRowsPerWg + rbase + threadIdx.x;
-        float mx = -INFINITY;
-        for (int k = 0; k < ns; ++k) mx = fmaxf(mx, lse[(size_t)k * kRowsPerWg]);
-        float den = 0.f;
-        for (int k = 0; k < ns; ++k) {
-            const float w = __builtin_amdgcn_exp2f(lse[(size_t)k * kRowsPerWg] - mx);
-            wgt[k][threadIdx.x] = w;
-            den += w;
-        }
-        inv_den[threadIdx.x] = 1.0f / den;
-    }
-    __syncthreads();
+    weights();
     for (int e = threadIdx.x; e < n_el; e += kAttnThreads) {
         const int rr = e / per_row;
-        const int d0 = (e % per_row) * 4;
         const float* src = src_of(e);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        auto add = [&](float w, const f32x4& v) {
-            acc.x += w * v[0];
-            acc.y += w * v[1];
-            acc.z += w * v[2];
-            acc.w += w * v[3];
-        };
-        // the splits' loads are issued eight at a time before any of them
-        // is used, so a unit of a few pieces waits for one round trip
         for (int k0 = 0; k0 < ns; k0 += kInFlight) {
             f32x4 v[kInFlight];
             if (k0 == 0 && e == (int)threadIdx.x) {
@@ -1192,13 +1246,9 @@ combine_kernel(PackView pv, AttnWs ws, T* __restrict__ out, int Hq, int Hkv,
             }
 #pragma unroll
             for (int j = 0; j < kInFlight; ++j)
-                if (k0 + j < ns) add(wgt[k0 + j][rr], v[j]);
+                if (k0 + j < ns) add(acc, wgt[k0 + j][rr], v[j]);
         }
-        const float id = inv_den[rr];
-        const int r = rg * kRowsPerWg + rbase + rr;
-        const int pos_local = r / g, hg = r % g;
-        T* dst = out + ((size_t)(row0 + pos_local) * Hq + c * g + hg) * D + d0;
-        store_out4<T>(dst, make_float4(acc.x * id, acc.y * id, acc.z * id, acc.w * id));
+        store(e, acc);
     }
 }
 
