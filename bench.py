@@ -55,10 +55,14 @@ def parse_args():
     ap.add_argument("--no-loop", action="store_true",
                     help="skip the whole-decode loop runs on the synthetic model")
     ap.add_argument("--plan-overlap", action="store_true",
-                    help="run the attention's plan (fb_attention_plan) on a second stream "
-                         "beside the window KV write, then fb_wavefront_attention_planned "
-                         "(measured: 0.8-1.6%% faster under graph replay, equal or slower "
-                         "eager, where the cross-stream events cost more than the plan)")
+                    help="run the eager loop's steps, too, with the attention's plan "
+                         "(fb_attention_plan) on a second stream beside the window KV write, "
+                         "then fb_wavefront_attention_planned, as the graph's steps are by "
+                         "default (eager it measured equal or slower: the cross-stream events "
+                         "cost more than the plan)")
+    ap.add_argument("--graph-one-call", action="store_true",
+                    help="capture the graph's steps with the one-call attention instead of "
+                         "the plan beside the window KV write")
     ap.add_argument("--no-lmhead", action="store_true",
                     help="skip the LM head with the fused vocabulary reduction")
     ap.add_argument("--lmhead-dim", type=int, default=2048,
@@ -268,11 +272,13 @@ def hbm_probe(torch, fb, nbytes=2 << 30, reps=5, logits=None):
     return res
 
 
-def graph_replay(torch, fb, step, one_step, copies, K, W):
+def graph_replay(torch, fb, step, one_step, copies, K, W, split=True):
     """The same K steps captured once in a HIP graph and replayed.
 
     Each captured step works on its own pristine copy of the request state,
-    as in the eager loop.  A warm-up replay runs first, the copies are
+    as in the eager loop.  With `split` the attention runs in its two-call
+    form, its plan on a second stream beside the window KV write (a fork and
+    join inside the graph, with no event cost at replay).  A warm-up replay runs first, the copies are
     restored outside the graph, then one timed replay between two
     synchronizations (wall clock, as the eager loop; the HIP-event interval
     of the replay is reported beside it).  Its outputs (last step's attention
@@ -286,7 +292,7 @@ def graph_replay(torch, fb, step, one_step, copies, K, W):
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         for i in range(K):
-            one_step(0, None, gcopies[i])
+            one_step(0, None, gcopies[i], overlap=split)
 
     def restore():
         for c in gcopies:
@@ -310,7 +316,7 @@ def graph_replay(torch, fb, step, one_step, copies, K, W):
         all(torch.equal(a, b) for a, b in zip(gcopies[K - 1], ref[:4]))
     return {"ms_per_step": wall_ms if same else None,
             "ms_per_step_events": ms if same else None, "matches_eager": bool(same),
-            "steps_per_replay": K}
+            "steps_per_replay": K, "plan_beside_kv_write": bool(split)}
 
 
 def prologue_bench(torch, fb, step, t, reps=20):
@@ -444,7 +450,7 @@ def loop_bench(torch, fb, synth, DecodeLoop):
 
 
 def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
-                 cold=True, plan_overlap=False):
+                 cold=True, plan_overlap=False, graph_split=True):
     """K timed steps of one workload (after W warm-up steps), each on its own
     copy of the pristine request state.  Returns (result dict, context for the
     sections that reuse the step's buffers)."""
@@ -470,14 +476,15 @@ def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
     side = torch.cuda.Stream()
     packed, planned = torch.cuda.Event(), torch.cuda.Event()
 
-    def one_step(i, ev, state=None):
+    def one_step(i, ev, state=None, overlap=None):
+        split = plan_overlap if overlap is None else overlap
         st, tok, pe, fin = copies[i] if state is None else state
         if ev is not None:
             ev[0].record()
         fb.fb_pack_wavefronts(st, tok, step.n_max, step.T_max, step.pack)
         if ev is not None:
             ev[1].record()
-        if plan_overlap:
+        if split:
             packed.record(main)
             side.wait_event(packed)
             fb.fb_attention_plan(step.pack, step.shape, step.attn_ws, side)
@@ -486,7 +493,7 @@ def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
                               step.page_table, step.pack, step.shape)
         if ev is not None:
             ev[2].record()
-        if plan_overlap:
+        if split:
             main.wait_event(planned)
             fb.fb_wavefront_attention_planned(t["q"], t["k_cache"], t["v_cache"],
                                               step.page_table, step.pack, step.shape,
@@ -521,7 +528,8 @@ def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
                             for i in range(K)])) for j, n in enumerate(names)}
     ms_step = wall * 1e3 / K
     step_ms = [events[i][0].elapsed_time(events[i][nph]) for i in range(K)]
-    gr = graph_replay(torch, fb, step, one_step, copies, K, W) if graph else None
+    gr = (graph_replay(torch, fb, step, one_step, copies, K, W, graph_split)
+          if graph else None)
     cd = cold_steps(torch, one_step, step, K, nph) if cold else None
     t_attn = ph["attention"] * 1e-3
     t_voc = ph["vocab_reduce"] * 1e-3
@@ -601,7 +609,7 @@ def main():
     overlap = args.plan_overlap
     head, ctx = measure_step(torch, fb, synth, WavefrontStep, args.workload, args.seed,
                              K, W, graph=not args.no_graph, cold=not args.no_cold,
-                             plan_overlap=overlap)
+                             plan_overlap=overlap, graph_split=not args.graph_one_call)
     wl, host, t, step, n_live = (ctx[k] for k in ("wl", "host", "t", "step", "n_live"))
     out = {
         "metric": METRIC,
@@ -637,7 +645,8 @@ def main():
     if args.second and args.second != args.workload:
         sec, sctx = measure_step(torch, fb, synth, WavefrontStep, args.second, args.seed,
                                  K, W, graph=not args.no_graph, cold=not args.no_cold,
-                                 plan_overlap=overlap)
+                                 plan_overlap=overlap,
+                                 graph_split=not args.graph_one_call)
         out[args.second] = sec
         del sctx
         torch.cuda.empty_cache()
