@@ -18,7 +18,8 @@
 //                  and the list of split units
 //   attn_bf16      one workgroup (4 waves x 32 rows) per item: 32-key K and
 //                  V^T tiles streamed through an LDS ring (3 stages at
-//                  D = 128, 4 below) by direct global->LDS loads,
+//                  D = 128, K refilled a step ahead of V^T; 4 below) by
+//                  direct global->LDS loads,
 //                  S^T = K Q^T and O^T += V^T P^T on
 //                  v_mfma_f32_32x32x16_bf16, online softmax in the exp2
 //                  domain with lazy rescaling
@@ -941,8 +942,10 @@ attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_
         const int p0 = FAST ? tile_page(kt0) : 0;
         const int p1 = (FAST && nt > 1) ? tile_page(kt0 + 1) : 0;
         const int p2 = (FAST && nt > 2) ? tile_page(kt0 + 2) : 0;
-        // K(0), K(1), V^T(0), then Q; the first wait lets the later ring
-        // loads stay in flight (Q is waited for where it is used)
+        // K(0), K(1), V^T(0), then Q.  The explicit wait is for K(0) alone
+        // (it does not count on Q's loads, which a wave without valid rows
+        // skips); Q is waited for where it is used, and as loads complete in
+        // order that wait covers K(1) and V^T(0) too.
         issue_part(kt0, C0{}, p0, KPart{});
         if (nt > 1) issue_part(kt0 + 1, C1{}, p1, KPart{});
         issue_part(kt0, C0{}, p0, VPart{});
