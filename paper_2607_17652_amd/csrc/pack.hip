@@ -4,9 +4,12 @@
 //
 // pack_kernel (one workgroup) validates every request and computes w_b; a
 // block-wide exclusive scan of w_b gives each request its first tile (and, in
-// the ragged layout, its first packed row).  rowmap_kernel then writes every
-// one of the row_cap row-map entries exactly once, live or not, so the output
-// is fully defined without a separate clearing pass.
+// the ragged layout, its first packed row).  Then every one of the row_cap
+// row-map entries is written exactly once, live or not, so the output is
+// fully defined without a separate clearing pass: by the same workgroup from
+// the (request, first position) of each tile (ragged) or (w_b, o_b) of each
+// request (padded) it kept in LDS, or, when there are more of those than the
+// LDS copy holds, by rowmap_kernel, one thread per row.
 #include "internal.h"
 
 namespace fb {
@@ -41,11 +44,20 @@ __device__ int workgroup_exclusive_scan(int v, int* lds, int* total) {
     return (wave > 0 ? before : 0) + x - v;
 }
 
+// Tiles (ragged) or requests (padded) whose row-map inputs the pack keeps in
+// LDS to write the row maps itself.
+constexpr int kFusedMax = 4096;
+
+template <bool ROWS>
 __global__ void __launch_bounds__(kPackThreads)
 pack_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tokens,
             int B, int W_max, int bl, int layout, int n_max, int T_max,
             PackView pv, int row_cap) {
     __shared__ int scan_lds[kPackWaves + 1];
+    // ragged: request and first position of each tile; padded: w_b (-1 for a
+    // bad state) and o_b of each request
+    __shared__ int s_a[ROWS ? kFusedMax : 1];
+    __shared__ int s_b[ROWS ? kFusedMax : 1];
     const int tid = threadIdx.x;
     if (tid == 0) pv.hdr[kHdrStatus] = FB_PACK_STATUS_NONE;
     __syncthreads();
@@ -77,7 +89,15 @@ pack_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tok
             pv.req_row0[b] = row0;
             if (bad) record_error(pv.hdr, b, FB_DERR_STATE);
             const int o = s.gen_start + s.L * bl;
+            if (ROWS && layout == FB_PADDED) {
+                s_a[b] = bad ? -1 : w;
+                s_b[b] = o;
+            }
             for (int sl = 0; sl < w; ++sl) {
+                if (ROWS && layout != FB_PADDED) {
+                    s_a[tile0 + sl] = b;
+                    s_b[tile0 + sl] = o + sl * bl;
+                }
                 int32_t* t = pv.tiles + (size_t)(tile0 + sl) * kTileInts;
                 t[kTB] = b;
                 t[kTS] = sl;
@@ -94,6 +114,48 @@ pack_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ tok
     if (tid == 0) {
         pv.hdr[kHdrRows] = tiles_before * bl;
         pv.hdr[kHdrTiles] = tiles_before;
+    }
+    if constexpr (ROWS) {
+        // ---- phase 2: the row maps (as rowmap_kernel), four rows per
+        // thread and pass with their token loads in flight together
+        __syncthreads();
+        const int n_rows = tiles_before * bl;
+        const int q = W_max * bl;
+        constexpr int U = 4;
+        for (int r0 = tid; r0 < row_cap; r0 += U * kPackThreads) {
+            int rb[U], rp[U], rt[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int r = r0 + u * kPackThreads;
+                int b = -1, pos = -1;
+                if (r < row_cap) {
+                    if (layout == FB_PADDED) {
+                        const int req = r / q;
+                        if ((r % q) / bl < s_a[req]) {
+                            b = req;
+                            pos = s_b[req] + r % q;
+                        }
+                    } else if (r < n_rows) {
+                        b = s_a[r / bl];
+                        pos = s_b[r / bl] + r % bl;
+                    }
+                }
+                rb[u] = b;
+                rp[u] = pos;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                rt[u] = (rb[u] >= 0 && tokens) ? tokens[(size_t)rb[u] * T_max + rp[u]] : -1;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int r = r0 + u * kPackThreads;
+                if (r < row_cap) {
+                    pv.row_req[r] = rb[u];
+                    pv.row_pos[r] = rp[u];
+                    pv.row_tok[r] = rt[u];
+                }
+            }
+        }
     }
 }
 
@@ -134,7 +196,15 @@ rowmap_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ t
 hipError_t launch_pack(const fb_req_state* st, const int32_t* tokens, int n_max,
                        int T_max, const fb_pack* pack, hipStream_t stream) {
     PackView pv = pack_view(pack);
-    hipLaunchKernelGGL(pack_kernel, dim3(1), dim3(kPackThreads), 0, stream, st,
+    const bool rows = pack->layout == FB_PADDED ? pack->B <= kFusedMax
+                                                : pack->tile_cap <= kFusedMax;
+    if (rows) {
+        hipLaunchKernelGGL(pack_kernel<true>, dim3(1), dim3(kPackThreads), 0, stream, st,
+                           tokens, pack->B, pack->W_max, pack->bl, pack->layout,
+                           n_max, T_max, pv, pack->row_cap);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(pack_kernel<false>, dim3(1), dim3(kPackThreads), 0, stream, st,
                        tokens, pack->B, pack->W_max, pack->bl, pack->layout,
                        n_max, T_max, pv, pack->row_cap);
     hipError_t e = hipGetLastError();

@@ -117,6 +117,21 @@ def test_short_items_take_every_ring_tail(kv_split, ps):
                     prefix=("uniform", 20, 400), window=("uniform", 1, 3), prefix_jitter=13)
 
 
+@pytest.mark.parametrize("layout,B,W_max", [("ragged", 1000, 4), ("ragged", 1100, 4),
+                                            ("padded", 4000, 2), ("padded", 4100, 2)])
+def test_pack_row_maps_in_the_workgroup_and_beyond(layout, B, W_max):
+    """The pack writes the row maps itself while the tiles (ragged) or the
+    requests (padded) fit its LDS copy of 4096 and leaves them to a per-row
+    kernel beyond; both sides of each bound equal the oracle's Eq. 4 pack."""
+    wl, host, t, step = setup("tiny", B=B, W_max=W_max, layout=layout, V=64,
+                              prefix=("uniform", 8, 64), window=("uniform", 1, W_max),
+                              n_blocks=24)
+    log(f"[parity] pack only: layout={layout} B={B} W_max={W_max}")
+    step.pack_step()
+    torch.cuda.synchronize()
+    compare_pack(wl, host, gpu_results(step), host["tokens"])
+
+
 def test_explicit_kv_split_matches_oracle():
     run_and_compare("hetero64", reqs=list(range(0, 64, 7)), kv_split=256)
 
