@@ -219,6 +219,7 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
     uint8_t* s_flag = reinterpret_cast<uint8_t*>(s_xhat + rows_cap);
     __shared__ double s_rho[64];
     __shared__ int s_m2t[64], s_t2t[64];
+    __shared__ uint8_t s_fin[64];   // fin of the live blocks after this step
 
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
@@ -336,13 +337,17 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
             const int g = s.L + sl;
             uint8_t* pe_g = pe + (size_t)b * n_max + g;
             uint8_t* fin_g = fin + (size_t)b * n_max + g;
+            const uint8_t fin0 = *fin_g;
+            bool now = false;
             if (m_before == 0) {
                 const int npe = min(255, (int)*pe_g + 1);
                 *pe_g = (uint8_t)npe;
-                if (u == 0 || npe >= prm.S_pe) *fin_g = 1;
+                now = u == 0 || npe >= prm.S_pe;
             } else if (m_after == 0 && prm.S_pe == 0) {
-                *fin_g = 1;
+                now = true;
             }
+            if (now) *fin_g = 1;
+            s_fin[sl] = (fin0 || now) ? 1 : 0;
             s_rho[sl] = m_before == 0 ? 1.0 : (double)dec / (double)m_before;
             s_m2t[sl] = wr_masked;
             s_t2t[sl] = u - wr_masked;
@@ -368,8 +373,8 @@ request_kernel(const float4* __restrict__ part, int nsplit, PackView pv,
     }
     fb_req_state ns = s;
     if (ns.active) {
-        const uint8_t* fin_b = fin + (size_t)b * n_max;
-        while (ns.L < ns.R && fin_b[ns.L]) {
+        // every block in [L, R) is live this step, so its fin is in s_fin
+        while (ns.L < ns.R && s_fin[ns.L - s.L]) {
             const int g = ns.L;
             ns.L += 1;
             rs.committed += 1;
