@@ -6,10 +6,10 @@
 // block-wide exclusive scan of w_b gives each request its first tile (and, in
 // the ragged layout, its first packed row).  Then every one of the row_cap
 // row-map entries is written exactly once, live or not, so the output is
-// fully defined without a separate clearing pass: by the same workgroup from
-// the (request, first position) of each tile (ragged) or (w_b, o_b) of each
-// request (padded) it kept in LDS, or, when there are more of those than the
-// LDS copy holds, by rowmap_kernel, one thread per row.
+// fully defined without a separate clearing pass: for up to 4096 rows by the
+// same workgroup, from the (request, first position) of each tile (ragged)
+// or (w_b, o_b) of each request (padded) it kept in LDS; beyond, by
+// rowmap_kernel, one thread per row.
 #include "internal.h"
 
 namespace fb {
@@ -45,8 +45,11 @@ __device__ int workgroup_exclusive_scan(int v, int* lds, int* total) {
 }
 
 // Tiles (ragged) or requests (padded) whose row-map inputs the pack keeps in
-// LDS to write the row maps itself.
+// LDS to write the row maps itself, and the row maps one workgroup writes
+// faster than a separate launch (measured: 1024 rows 10.7 -> 8.5 us, 32768
+// rows 11 -> 20 us).
 constexpr int kFusedMax = 4096;
+constexpr int kFusedRows = 4096;
 
 template <bool ROWS>
 __global__ void __launch_bounds__(kPackThreads)
@@ -196,8 +199,9 @@ rowmap_kernel(const fb_req_state* __restrict__ st, const int32_t* __restrict__ t
 hipError_t launch_pack(const fb_req_state* st, const int32_t* tokens, int n_max,
                        int T_max, const fb_pack* pack, hipStream_t stream) {
     PackView pv = pack_view(pack);
-    const bool rows = pack->layout == FB_PADDED ? pack->B <= kFusedMax
-                                                : pack->tile_cap <= kFusedMax;
+    const bool rows = pack->row_cap <= kFusedRows &&
+                      (pack->layout == FB_PADDED ? pack->B <= kFusedMax
+                                                 : pack->tile_cap <= kFusedMax);
     if (rows) {
         hipLaunchKernelGGL(pack_kernel<true>, dim3(1), dim3(kPackThreads), 0, stream, st,
                            tokens, pack->B, pack->W_max, pack->bl, pack->layout,

@@ -117,12 +117,13 @@ def test_short_items_take_every_ring_tail(kv_split, ps):
                     prefix=("uniform", 20, 400), window=("uniform", 1, 3), prefix_jitter=13)
 
 
-@pytest.mark.parametrize("layout,B,W_max", [("ragged", 1000, 4), ("ragged", 1100, 4),
-                                            ("padded", 4000, 2), ("padded", 4100, 2)])
+@pytest.mark.parametrize("layout,B,W_max", [("ragged", 256, 4), ("ragged", 257, 4),
+                                            ("padded", 512, 2), ("padded", 513, 2),
+                                            ("ragged", 1100, 4)])
 def test_pack_row_maps_in_the_workgroup_and_beyond(layout, B, W_max):
-    """The pack writes the row maps itself while the tiles (ragged) or the
-    requests (padded) fit its LDS copy of 4096 and leaves them to a per-row
-    kernel beyond; both sides of each bound equal the oracle's Eq. 4 pack."""
+    """The pack writes the row maps itself up to 4096 rows (B*W_max*bl, bl = 4
+    here) and leaves them to a per-row kernel beyond; both sides of the bound,
+    in both layouts, equal the oracle's Eq. 4 pack."""
     wl, host, t, step = setup("tiny", B=B, W_max=W_max, layout=layout, V=64,
                               prefix=("uniform", 8, 64), window=("uniform", 1, W_max),
                               n_blocks=24)
