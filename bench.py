@@ -528,8 +528,17 @@ def measure_step(torch, fb, synth, WavefrontStep, name, seed, K, W, graph=True,
                             for i in range(K)])) for j, n in enumerate(names)}
     ms_step = wall * 1e3 / K
     step_ms = [events[i][0].elapsed_time(events[i][nph]) for i in range(K)]
-    gr = (graph_replay(torch, fb, step, one_step, copies, K, W, graph_split)
-          if graph else None)
+    gr = None
+    if graph:
+        try:
+            gr = graph_replay(torch, fb, step, one_step, copies, K, W, graph_split)
+        except Exception as exc:   # capture unavailable: the eager loop is the headline
+            try:
+                torch.cuda.synchronize()
+            except Exception:
+                pass
+            print(f"[bench] graph replay skipped: {exc!r}", file=sys.stderr, flush=True)
+            gr = {"ms_per_step": None, "matches_eager": False, "error": repr(exc)}
     cd = cold_steps(torch, one_step, step, K, nph) if cold else None
     t_attn = ph["attention"] * 1e-3
     t_voc = ph["vocab_reduce"] * 1e-3
