@@ -12,6 +12,7 @@ import torch
 from harness import (OracleCase, compare_case, compare_pack, gpu_results, log,
                      setup)
 from paper_2607_17652_amd import binding as fb
+from paper_2607_17652_amd import synth
 
 pytestmark = pytest.mark.gpu
 
@@ -131,6 +132,16 @@ def test_pack_row_maps_in_the_workgroup_and_beyond(layout, B, W_max):
     step.pack_step()
     torch.cuda.synchronize()
     compare_pack(wl, host, gpu_results(step), host["tokens"])
+
+
+@pytest.mark.parametrize("name,seed,stride", [("long8", 1, 1), ("hetero64", 2, 3),
+                                             ("serve256", 1, 9), ("single", 4, 1)])
+def test_other_seeds(name, seed, stride):
+    """Other draws of the same workloads (request mixes, prefix lengths and
+    so item lengths, page permutations, logits), every stride-th request
+    compared."""
+    wl = synth.workload(name)
+    run_and_compare(name, reqs=list(range(seed % stride, wl.B, stride)), seed=seed)
 
 
 def test_explicit_kv_split_matches_oracle():
